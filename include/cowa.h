@@ -1,0 +1,170 @@
+/*
+ * cowa.h -- C ABI of the CoWindow Attention (CoWA) library for AMD MI355X (gfx950).
+ *
+ * CoWA is causal attention in which every KV head sees a shared prefix-sink
+ * window and a shared near-diagonal window, while complementary long-range
+ * windows split the remaining causal distances across the KV heads so that
+ * together they cover the whole causal prefix (paper Sec. 2.1, Eq. fwa_support,
+ * Eq. fwa_collective_coverage).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - All functions are extern "C", never throw, and return a cowa_status.  On a
+ *   negative status nothing has been launched and no output has been written;
+ *   cowa_last_error() then returns a message for the calling thread.
+ * - Device pointers are plain addresses of memory the caller allocated on the
+ *   current HIP device.  The library allocates no memory, never synchronises,
+ *   and enqueues its kernels on the given stream (a hipStream_t passed as
+ *   void*; NULL is the default stream).  Asynchronous kernel faults surface at
+ *   the caller's next synchronisation of that stream.
+ * - Tensors are dense, contiguous and head-major (Sec. 2.3, forward
+ *   execution): Q, O, dQ, dO are [B, H_q, N_q, d]; K, V, dK, dV are
+ *   [B, H_k, N_k, d]; LSE is [B, H_q, N_q] float32 holding the natural-log
+ *   log-sum-exp of each row (Alg. 1, final step).  Element type is bfloat16 or
+ *   float32 per cowa_params.dtype; q/k/v/o/do/dq/dk/dv must be 16-byte aligned
+ *   and lse 4-byte aligned.
+ * - Queries and keys are bottom-right aligned: query i_q and key i_k are at
+ *   causal distance delta = i_q + (N_k - N_q) - i_k (Eq. fwa_distance); N_q <= N_k.
+ * - QO head h uses KV head floor(h * H_k / H_q) (Sec. 2.1, grouped-query attention).
+ * - Window breakpoints use the global KV-head index h_k_offset + h_local and the
+ *   global head count h_k_total (Eq. fwa_global_head); a single device holding
+ *   all heads passes h_k_total = h_k and h_k_offset = 0.
+ */
+#ifndef COWA_H_
+#define COWA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  COWA_OK = 0,
+  COWA_ERR_INVALID_ARG = -1,       /* a size, window, pointer or alignment is invalid */
+  COWA_ERR_UNSUPPORTED = -2,       /* valid but not built: head_dim, tile or dtype combination */
+  COWA_ERR_WORKSPACE = -3,         /* workspace pointer missing or smaller than required */
+  COWA_ERR_SCHEDULE_MISMATCH = -4, /* schedule built for different shapes or windows */
+  COWA_ERR_NO_DEVICE = -5,         /* no HIP device, or the current device is not gfx950 */
+  COWA_ERR_HIP = -6                /* a HIP call or kernel launch failed */
+} cowa_status;
+
+typedef enum { COWA_BF16 = 0, COWA_FP32 = 1 } cowa_dtype;
+
+/* Per-KV-head window four-tuple of Sec. 2.1: (sink width, near width, gap
+ * after the near window, long-range width) = (w_sink, w_near, b_h, b_{h+1} - b_h),
+ * with L = max(N_k - w_sink - w_near, 0) and b_h = floor(h L / H_k)
+ * (Eq. fwa_long_range_span). */
+typedef struct {
+  int32_t sink, near, gap, width;
+} cowa_window;
+
+/* Shapes and windows of one forward/backward call. */
+typedef struct {
+  int32_t batch;          /* B >= 0; B = 0 is a no-op */
+  int32_t n_q, n_k;       /* 1 <= N_q <= N_k < 2^30 */
+  int32_t h_q, h_k;       /* local heads on this device; H_q % H_k == 0 */
+  int32_t head_dim;       /* 64 or 128 */
+  int32_t w_sink, w_near; /* >= 0 */
+  int32_t h_k_total;      /* global KV heads (>= h_k_offset + h_k) */
+  int32_t h_k_offset;     /* global index of local KV head 0 */
+  int32_t tile_q, tile_k; /* block sizes B_q, B_k: 32, 64 or 128 */
+  float softmax_scale;    /* multiplies Q K^T (1/sqrt(d) for the standard scale) */
+  int32_t dtype;          /* cowa_dtype */
+} cowa_params;
+
+/* Block schedule (Sec. 2.3): for every local KV head h and QO block i the KV
+ * blocks J_h(i) that hold at least one legal pair, and its inverse I_h(j).
+ * A caller-owned plain struct; the device buffer `buf` of `bytes` bytes is
+ * caller-allocated and filled by cowa_schedule().  Layout of buf (each array
+ * starts at a 256-byte aligned offset given below):
+ *   fwd_row_ptr  int32 [h_k * n_qt + 1]   row r = h * n_qt + i
+ *   bwd_col_ptr  int32 [h_k * n_kt + 1]   column c = h * n_kt + j
+ *   fwd_ent      uint32[nnz]  (j << 1) | partial, j descending in a row (Alg. 1)
+ *   bwd_ent      uint32[nnz]  (i << 1) | partial, i ascending in a column (Alg. 2)
+ * partial = 0 (FULL) iff all B_q * B_k element pairs of the tile lie inside
+ * both sequences and are legal; only partial tiles are masked element-wise. */
+typedef struct {
+  cowa_params p;          /* the parameters it was sized for */
+  int32_t n_qt, n_kt;     /* ceil(N_q / B_q), ceil(N_k / B_k) */
+  int32_t max_row;        /* longest J_h(i) */
+  int32_t max_col;        /* longest I_h(j) */
+  int64_t nnz;            /* listed tiles over the local KV heads */
+  size_t off_fwd_row_ptr, off_bwd_col_ptr, off_fwd_ent, off_bwd_ent; /* byte offsets in buf */
+  size_t bytes;           /* size of buf */
+  void* buf;              /* device buffer, set by the caller */
+} cowa_schedule_t;
+
+/* Shapes of one decoding step (Sec. 2.3, decoding execution). */
+typedef struct {
+  int32_t batch;          /* sequences B >= 0 */
+  int32_t h_q, h_k;       /* local heads; H_q % H_k == 0 */
+  int32_t head_dim;       /* 64 or 128 */
+  int32_t n_max;          /* KV-cache capacity (row stride) per sequence and head */
+  int32_t w_sink, w_near; /* >= 0 */
+  int32_t h_k_total, h_k_offset;
+  int32_t split_keys;     /* visible keys per split program; 0 = library default */
+  float softmax_scale;
+  int32_t dtype;          /* COWA_BF16 or COWA_FP32 */
+} cowa_decode_params;
+
+/* Library version string. */
+const char* cowa_version(void);
+
+/* Message for the last non-OK status returned on the calling thread. */
+const char* cowa_last_error(void);
+
+/* Window tuples of the h_k local KV heads for key length n_k (Sec. 2.1,
+ * Eq. fwa_long_range_span, Eq. fwa_global_head).  Host only; out_host has
+ * p->h_k entries.  Computed in 64-bit integers. */
+cowa_status cowa_windows(const cowa_params* p, cowa_window* out_host);
+
+/* Size the schedule of `p` (Sec. 2.3; tile sets are the paper's J_h(i) and
+ * I_h(j)): fills every field of *out except buf.  Host only, O(h_k (n_qt + n_kt)). */
+cowa_status cowa_schedule_size(const cowa_params* p, cowa_schedule_t* out);
+
+/* Build the schedule into s->buf on the device (three small kernels:
+ * per-row counts, prefix sums, entry fill). */
+cowa_status cowa_schedule(const cowa_schedule_t* s, void* stream);
+
+/* Forward (Alg. 1): O and LSE of masked softmax attention over each query's
+ * visible-key set.  q [B,H_q,N_q,d], k/v [B,H_k,N_k,d] -> o [B,H_q,N_q,d],
+ * lse [B,H_q,N_q] float32.  `s` must have been sized for the same n_q, n_k,
+ * h_k, windows, global head indexing and tiles, and built. */
+cowa_status cowa_fwd(const cowa_params* p, const cowa_schedule_t* s,
+                     const void* q, const void* k, const void* v,
+                     void* o, float* lse, void* stream);
+
+/* Workspace bytes cowa_bwd needs: the float32 dQ accumulator and the row
+ * sums D = rowsum(O * dO). */
+cowa_status cowa_bwd_workspace_size(const cowa_params* p, size_t* bytes);
+
+/* Backward (Alg. 2): exact gradients of <dO, O> w.r.t. the unscaled Q, K and
+ * V, using the saved O and LSE of the forward.  dq like q; dk/dv like k/v
+ * (keys that no query sees get zero).  bf16 only. */
+cowa_status cowa_bwd(const cowa_params* p, const cowa_schedule_t* s,
+                     const void* q, const void* k, const void* v,
+                     const void* o, const float* lse, const void* d_o,
+                     void* dq, void* dk, void* dv,
+                     void* workspace, size_t ws_bytes, void* stream);
+
+/* Workspace bytes of one decoding step: split partial states (m, l, O). */
+cowa_status cowa_decode_workspace_size(const cowa_decode_params* p, size_t* bytes);
+
+/* One decoding step (Sec. 2.3): the forward with N_q = 1 for every sequence b,
+ * N_k = seqlens_k[b] (cached tokens plus the current one, already appended;
+ * 1 <= N_k <= n_max), breakpoints recomputed from that N_k.  q [B,H_q,d],
+ * k_cache/v_cache [B,H_k,n_max,d], seqlens_k device int32 [B] -> o [B,H_q,d],
+ * lse [B,H_q].  A seqlens_k value outside [1, n_max] yields O = 0 and
+ * LSE = -inf for that sequence. */
+cowa_status cowa_decode(const cowa_decode_params* p, const void* q,
+                        const void* k_cache, const void* v_cache,
+                        const int32_t* seqlens_k, void* o, float* lse,
+                        void* workspace, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COWA_H_ */

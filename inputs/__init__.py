@@ -72,7 +72,7 @@ def seed_sequence(workload_key, tensor):
     if isinstance(workload_key, str):
         workload_key = _WORKLOAD_KEYS.get(workload_key, None) if workload_key in _WORKLOAD_KEYS \
             else key_of(workload_key)
-    return np.random.SeedSequence(42, spawn_key=(int(workload_key), _TENSOR_KEYS.get(tensor, 99)))
+    return np.random.SeedSequence(42, spawn_key=(int(workload_key), _TENSOR_KEYS.get(tensor, key_of(tensor))))
 
 
 def f32_to_bf16_bits(x):

@@ -1,0 +1,295 @@
+// CoWA decoding step (Sec. 2.3, decoding execution): the forward with N_q = 1,
+// N_k = seqlens_k[b], breakpoints recomputed from that N_k.
+//
+// Split kernel: one workgroup per (split s, local KV head h, sequence b).  The
+// visible keys of (b, h) are the merged key runs of sink, long-range window and
+// near window; split s takes positions [s * SK, (s + 1) * SK) of that ascending
+// list.  Loads are 16-byte and coalesced: a 64-lane wave reads whole K and V
+// rows (d/8 lanes per row), so every wave step streams a contiguous run of
+// cache rows.  Each lane group keeps, for each of the G QO heads of the group,
+// an online-softmax state (m, l, O slice) in registers; the workgroup merges
+// its 4 x (64 / (d/8)) states and writes one partial (m, l, O) per QO head.
+//
+// Combine kernel: one 64-lane wave per (sequence, QO head) merges the split
+// partials (max of m, rescaled sums) and writes O and the natural-log LSE.
+// Everything is fp32 apart from the bf16 loads; scores are kept in base 2.
+#include "internal.h"
+#include "window_rule.h"
+
+namespace cowa {
+namespace {
+
+constexpr int kDefaultSplitKeys = 512;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr int kUnroll = 4;  // key steps in flight per lane group
+
+struct DecArgs {
+  const __bf16* q;
+  const __bf16* kc;
+  const __bf16* vc;
+  const int32_t* seqlens;
+  __bf16* o;
+  float* lse;
+  float* part_o;   // [B][H_q][S][D]
+  float* part_ml;  // [B][H_q][S][2]
+  int32_t batch, h_q, h_k, n_max, w_sink, w_near, h_total, h_offset, splits, split_keys;
+  float c;  // softmax_scale * log2(e)
+};
+
+__device__ inline void bf16x8_to_f32(const uint4& w, float* f) {
+  const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    f[2 * t] = __uint_as_float(ws[t] << 16);
+    f[2 * t + 1] = __uint_as_float(ws[t] & 0xffff0000u);
+  }
+}
+
+template <int D, int G>
+__global__ void __launch_bounds__(256) decode_split(DecArgs a) {
+  constexpr int DC = D / 8;     // lanes per cache row
+  constexpr int KG = 64 / DC;   // rows per wave step
+  __shared__ float sm_m[4][G], sm_l[4][G];
+  __shared__ float sm_o[4][G][D];
+
+  const int s = blockIdx.x, hk = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int kg = lane / DC, dc = lane % DC;
+
+  const int32_t n_k = a.seqlens[b];
+  const bool valid = n_k >= 1 && n_k <= a.n_max;
+  Ranges runs;
+  runs.n = 0;
+  int32_t total = 0;
+  if (valid) {
+    int64_t lo, hi;
+    long_bounds(n_k, a.w_sink, a.w_near, (int64_t)a.h_offset + hk, a.h_total, &lo, &hi);
+    runs = decode_key_runs(n_k, a.w_sink, a.w_near, lo, hi);
+    total = ranges_count(runs);
+  }
+  const int32_t v0 = s * a.split_keys;
+  const int32_t v1 = min(v0 + a.split_keys, total);
+
+  // query slices of the G QO heads, pre-scaled by scale * log2(e)
+  float qv[G][8];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const uint4 w = *reinterpret_cast<const uint4*>(a.q + ((int64_t)b * a.h_q + hk * G + g) * D + dc * 8);
+    bf16x8_to_f32(w, qv[g]);
+#pragma unroll
+    for (int t = 0; t < 8; ++t) qv[g][t] *= a.c;
+  }
+  float m[G], l[G], acc[G][8];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    m[g] = -INFINITY;
+    l[g] = 0.f;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) acc[g][t] = 0.f;
+  }
+
+  const int64_t head_off = ((int64_t)b * a.h_k + hk) * a.n_max * D;
+  const __bf16* kbase = a.kc + head_off + dc * 8;
+  const __bf16* vbase = a.vc + head_off + dc * 8;
+  constexpr int BLOCK_STEP = 4 * KG;  // rows per workgroup step
+
+  for (int32_t vb = v0; vb < v1; vb += BLOCK_STEP * kUnroll) {
+    uint4 kr[kUnroll], vr[kUnroll];
+    bool ok[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int32_t vi = vb + u * BLOCK_STEP + wave * KG + kg;
+      ok[u] = vi < v1;
+      kr[u] = make_uint4(0, 0, 0, 0);
+      vr[u] = make_uint4(0, 0, 0, 0);
+      if (ok[u]) {
+        const int64_t key = run_key(runs, vi);
+        kr[u] = *reinterpret_cast<const uint4*>(kbase + key * D);
+        vr[u] = *reinterpret_cast<const uint4*>(vbase + key * D);
+      }
+    }
+    float sc[G][kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      float kf[8];
+      bf16x8_to_f32(kr[u], kf);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        float part = 0.f;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) part = fmaf(qv[g][t], kf[t], part);
+#pragma unroll
+        for (int off = 1; off < DC; off <<= 1) part += __shfl_xor(part, off);
+        sc[g][u] = ok[u] ? part : -INFINITY;
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      float mx = sc[g][0];
+#pragma unroll
+      for (int u = 1; u < kUnroll; ++u) mx = fmaxf(mx, sc[g][u]);
+      const float m_new = fmaxf(m[g], mx);
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;
+      const float alpha = __builtin_amdgcn_exp2f(m[g] - m_use);
+      l[g] *= alpha;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) acc[g][t] *= alpha;
+      m[g] = m_new;
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const float p = __builtin_amdgcn_exp2f(sc[g][u] - m_use);
+        l[g] += p;
+        float vf[8];
+        bf16x8_to_f32(vr[u], vf);
+#pragma unroll
+        for (int t = 0; t < 8; ++t) acc[g][t] = fmaf(p, vf[t], acc[g][t]);
+      }
+    }
+  }
+
+  // merge the KG lane groups of each wave (lanes dc, dc + DC, ... hold the same d slice)
+#pragma unroll
+  for (int off = DC; off < 64; off <<= 1) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float mo = __shfl_xor(m[g], off);
+      const float lo2 = __shfl_xor(l[g], off);
+      const float mm = fmaxf(m[g], mo);
+      const float mu = mm == -INFINITY ? 0.f : mm;
+      const float f1 = __builtin_amdgcn_exp2f(m[g] - mu), f2 = __builtin_amdgcn_exp2f(mo - mu);
+      l[g] = l[g] * f1 + lo2 * f2;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const float ao = __shfl_xor(acc[g][t], off);
+        acc[g][t] = acc[g][t] * f1 + ao * f2;
+      }
+      m[g] = mm;
+    }
+  }
+  // then the four waves through LDS
+  if (kg == 0) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      if (dc == 0) { sm_m[wave][g] = m[g]; sm_l[wave][g] = l[g]; }
+#pragma unroll
+      for (int t = 0; t < 8; ++t) sm_o[wave][g][dc * 8 + t] = acc[g][t];
+    }
+  }
+  __syncthreads();
+
+  const int64_t part_base = (((int64_t)b * a.h_q + hk * G) * a.splits + s);
+  for (int x = tid; x < G * D; x += 256) {
+    const int g = x / D, d = x % D;
+    float mm = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) mm = fmaxf(mm, sm_m[r][g]);
+    const float mu = mm == -INFINITY ? 0.f : mm;
+    float ov = 0.f, lv = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float f = __builtin_amdgcn_exp2f(sm_m[r][g] - mu);
+      ov = fmaf(sm_o[r][g][d], f, ov);
+      lv = fmaf(sm_l[r][g], f, lv);
+    }
+    const int64_t pidx = part_base + (int64_t)g * a.splits;  // [b][hk*G + g][s]
+    a.part_o[pidx * D + d] = ov;
+    if (d == 0) {
+      a.part_ml[pidx * 2] = mm;
+      a.part_ml[pidx * 2 + 1] = lv;
+    }
+  }
+}
+
+// One wave per (sequence, QO head); lanes own D/64 output elements each.
+template <int D>
+__global__ void __launch_bounds__(256) decode_combine(DecArgs a) {
+  constexpr int PER = D / 64;
+  const int wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int lane = threadIdx.x & 63;
+  if (wave >= a.batch * a.h_q) return;
+  const int64_t base = (int64_t)wave * a.splits;
+  float mm = -INFINITY;
+  for (int s = lane; s < a.splits; s += 64) mm = fmaxf(mm, a.part_ml[(base + s) * 2]);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) mm = fmaxf(mm, __shfl_xor(mm, off));
+  const float mu = mm == -INFINITY ? 0.f : mm;
+  float ov[PER], lv = 0.f;
+#pragma unroll
+  for (int t = 0; t < PER; ++t) ov[t] = 0.f;
+  for (int s = 0; s < a.splits; ++s) {
+    const float ms = a.part_ml[(base + s) * 2];
+    const float f = __builtin_amdgcn_exp2f(ms - mu);
+    lv = fmaf(a.part_ml[(base + s) * 2 + 1], f, lv);
+#pragma unroll
+    for (int t = 0; t < PER; ++t) ov[t] = fmaf(a.part_o[(base + s) * D + lane * PER + t], f, ov[t]);
+  }
+  const float inv = lv > 0.f ? 1.f / lv : 0.f;
+#pragma unroll
+  for (int t = 0; t < PER; ++t) a.o[(int64_t)wave * D + lane * PER + t] = (__bf16)(ov[t] * inv);
+  if (lane == 0) a.lse[wave] = lv > 0.f ? (mm + __log2f(lv)) * kLn2 : -INFINITY;
+}
+
+int32_t max_visible(const cowa_decode_params& p) {
+  const int64_t span = p.n_max - (int64_t)p.w_sink - p.w_near;
+  const int64_t width = span > 0 ? (span + p.h_k_total - 1) / p.h_k_total : 0;
+  const int64_t v = (int64_t)p.w_sink + p.w_near + width;
+  return (int32_t)(v < p.n_max ? v : p.n_max);
+}
+
+template <int D, int G>
+hipError_t launch_dg(const DecArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL((decode_split<D, G>), dim3(a.splits, a.h_k, a.batch), dim3(256), 0, stream, a);
+  const int waves = a.batch * a.h_q;
+  hipLaunchKernelGGL(decode_combine<D>, dim3((waves + 3) / 4), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int32_t decode_split_keys(const cowa_decode_params& p) {
+  return p.split_keys > 0 ? p.split_keys : kDefaultSplitKeys;
+}
+
+int32_t decode_num_splits(const cowa_decode_params& p) {
+  const int32_t sk = decode_split_keys(p);
+  const int32_t v = max_visible(p);
+  return v > 0 ? (v + sk - 1) / sk : 1;
+}
+
+size_t decode_workspace_bytes(const cowa_decode_params& p) {
+  const size_t parts = (size_t)p.batch * p.h_q * decode_num_splits(p);
+  const size_t o_bytes = (parts * p.head_dim * sizeof(float) + 255) & ~size_t(255);
+  return o_bytes + ((parts * 2 * sizeof(float) + 255) & ~size_t(255));
+}
+
+bool decode_supported(int head_dim, int group) {
+  return (head_dim == 64 || head_dim == 128) && (group == 1 || group == 2 || group == 4 || group == 8);
+}
+
+hipError_t launch_decode(const cowa_decode_params& p, const void* q, const void* k_cache, const void* v_cache,
+                         const int32_t* seqlens, void* o, float* lse, void* ws, hipStream_t stream) {
+  DecArgs a;
+  a.q = static_cast<const __bf16*>(q);
+  a.kc = static_cast<const __bf16*>(k_cache);
+  a.vc = static_cast<const __bf16*>(v_cache);
+  a.seqlens = seqlens;
+  a.o = static_cast<__bf16*>(o);
+  a.lse = lse;
+  a.batch = p.batch; a.h_q = p.h_q; a.h_k = p.h_k; a.n_max = p.n_max; a.w_sink = p.w_sink; a.w_near = p.w_near;
+  a.h_total = p.h_k_total; a.h_offset = p.h_k_offset;
+  a.splits = decode_num_splits(p);
+  a.split_keys = decode_split_keys(p);
+  a.c = p.softmax_scale * kLog2e;
+  const size_t parts = (size_t)p.batch * p.h_q * a.splits;
+  a.part_o = static_cast<float*>(ws);
+  a.part_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + ((parts * p.head_dim * sizeof(float) + 255) & ~size_t(255)));
+  const int G = p.h_q / p.h_k;
+#define COWA_DEC_CASE(D_, G_) if (p.head_dim == D_ && G == G_) return launch_dg<D_, G_>(a, stream);
+  COWA_DEC_CASE(128, 4) COWA_DEC_CASE(128, 1) COWA_DEC_CASE(128, 2) COWA_DEC_CASE(128, 8)
+  COWA_DEC_CASE(64, 4) COWA_DEC_CASE(64, 1) COWA_DEC_CASE(64, 2) COWA_DEC_CASE(64, 8)
+#undef COWA_DEC_CASE
+  return hipErrorInvalidValue;
+}
+
+}  // namespace cowa

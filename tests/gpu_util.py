@@ -1,0 +1,53 @@
+"""Helpers shared by the GPU parity tests (no test functions here)."""
+
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+# bf16 outputs: max |x - ref| <= 2e-2 and ||x - ref||_F / ||ref||_F <= 1e-2, per tensor;
+# fp32 outputs: both <= 1e-5.
+TOL = {"bf16": (2e-2, 1e-2), "fp32": (1e-5, 1e-5)}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+def to_dev(payload, dev):
+    """uint16 bf16 bits -> torch.bfloat16; float32 -> torch.float32."""
+    if payload.dtype == np.uint16:
+        return torch.from_numpy(np.ascontiguousarray(payload).view(np.int16)).view(torch.bfloat16).to(dev)
+    return torch.from_numpy(np.ascontiguousarray(payload)).to(dev)
+
+
+def to_host(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def compare(name, got, ref, dtype="bf16"):
+    """Assert the parity bar; returns (max_abs, rel_fro)."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (name, got.shape, ref.shape)
+    fin = np.isfinite(ref)
+    assert np.array_equal(np.isfinite(got), fin), f"{name}: non-finite pattern differs"
+    # -inf entries (empty rows) must match exactly
+    assert np.array_equal(got[~fin], ref[~fin]), f"{name}: non-finite values differ"
+    diff = np.abs(got[fin] - ref[fin])
+    max_abs = float(diff.max(initial=0.0))
+    denom = float(np.sqrt((ref[fin] ** 2).sum()))
+    rel = float(np.sqrt((diff ** 2).sum()) / denom) if denom > 0 else max_abs
+    a_tol, r_tol = TOL[dtype]
+    log(f"  {name}: max_abs={max_abs:.3e} rel_fro={rel:.3e}")
+    assert max_abs <= a_tol, f"{name}: max abs error {max_abs:.3e} > {a_tol}"
+    assert rel <= r_tol, f"{name}: relative Frobenius error {rel:.3e} > {r_tol}"
+    return max_abs, rel

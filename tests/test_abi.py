@@ -1,0 +1,184 @@
+"""The C ABI on the host: the library loads, exports every symbol the header
+declares, sizes schedules and windows like the oracle, and rejects invalid
+arguments with the documented status before touching any device.
+(No kernel is launched here.)"""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from conftest import ROOT
+from oracle import windows as ow, schedule as osched
+
+cowa = pytest.importorskip("paper_2609_32704_amd")
+abi = cowa._abi
+
+HEADER = os.path.join(ROOT, "include", "cowa.h")
+
+
+def _lib():
+    try:
+        return abi.lib()
+    except ImportError as e:
+        pytest.fail(f"library not built: {e}")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+char\s*\*|cowa_status)\s*(cowa_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("cowa_schedule", "cowa_fwd", "cowa_bwd", "cowa_decode", "cowa_schedule_size", "cowa_windows",
+              "cowa_bwd_workspace_size", "cowa_decode_workspace_size", "cowa_last_error", "cowa_version"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = _lib()
+    for n in declared_functions():
+        assert hasattr(lib, n), n
+    assert "gfx950" in abi.cowa_version()
+
+
+def test_struct_sizes_match_header_layout():
+    # int32 fields pack without padding; the schedule struct holds size_t offsets
+    assert ctypes.sizeof(abi.cowa_params) == 14 * 4
+    assert ctypes.sizeof(abi.cowa_decode_params) == 12 * 4
+    assert ctypes.sizeof(abi.cowa_window) == 16
+
+
+@pytest.mark.parametrize("n_k,ws,wn,ht,ho,hk", [(131072, 128, 4096, 8, 0, 8), (512, 16, 64, 2, 0, 2),
+                                                (100, 0, 0, 3, 1, 2), (5, 10, 10, 4, 0, 4),
+                                                (2 ** 30 - 1, 7, 9, 64, 60, 4)])
+def test_windows_match_oracle(n_k, ws, wn, ht, ho, hk):
+    p = cowa.make_params(1, 1, n_k, hk, hk, 128, ws, wn, 64, 64, h_k_total=ht, h_k_offset=ho)
+    got = cowa.windows(p)
+    assert got == [ow.window_tuple(n_k, ws, wn, ho + h, ht) for h in range(hk)]
+
+
+@pytest.mark.parametrize("case", [(512, 512, 32, 32, 16, 64, 2, 2, 0), (8192, 8192, 64, 64, 64, 1024, 8, 8, 0),
+                                  (333, 1000, 64, 128, 3, 77, 3, 5, 2), (1, 1, 32, 32, 0, 1, 1, 1, 0)])
+def test_schedule_size_matches_oracle(case):
+    n_q, n_k, tq, tk, ws, wn, hk, ht, ho = case
+    p = cowa.make_params(1, n_q, n_k, hk, hk, 128, ws, wn, tq, tk, h_k_total=ht, h_k_offset=ho)
+    s = abi.cowa_schedule_size(p)
+    ref = osched.build(n_q, n_k, tq, tk, ws, wn, hk, ht, ho)
+    assert s.nnz == len(ref["fwd_ent"])
+    assert s.n_qt == ref["n_qt"] and s.n_kt == ref["n_kt"]
+    assert s.max_row == int(np.diff(ref["fwd_row_ptr"]).max())
+    assert s.max_col == int(np.diff(ref["bwd_col_ptr"]).max())
+    for off in (s.off_fwd_row_ptr, s.off_bwd_col_ptr, s.off_fwd_ent, s.off_bwd_ent):
+        assert off % 256 == 0
+    assert s.bytes >= s.off_bwd_ent + 4 * s.nnz
+
+
+def _good():
+    return cowa.make_params(1, 256, 256, 4, 2, 128, 8, 32, 64, 64)
+
+
+def _status(fn, *args):
+    return fn(*args)
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("n_q", 300, abi.COWA_ERR_INVALID_ARG), ("n_q", 0, abi.COWA_ERR_INVALID_ARG),
+    ("h_q", 5, abi.COWA_ERR_INVALID_ARG), ("tile_q", 48, abi.COWA_ERR_INVALID_ARG),
+    ("tile_k", 256, abi.COWA_ERR_INVALID_ARG), ("w_sink", -1, abi.COWA_ERR_INVALID_ARG),
+    ("w_near", -5, abi.COWA_ERR_INVALID_ARG), ("h_k_offset", 1, abi.COWA_ERR_INVALID_ARG),
+    ("h_k_total", 1, abi.COWA_ERR_INVALID_ARG), ("head_dim", 96, abi.COWA_ERR_UNSUPPORTED),
+    ("dtype", 7, abi.COWA_ERR_INVALID_ARG), ("batch", -1, abi.COWA_ERR_INVALID_ARG),
+    ("softmax_scale", float("inf"), abi.COWA_ERR_INVALID_ARG),
+])
+def test_invalid_params_rejected_on_host(field, value, status):
+    lib = _lib()
+    p = _good()
+    setattr(p, field, value)
+    s = abi.cowa_schedule_t()
+    assert lib.cowa_schedule_size(ctypes.byref(p), ctypes.byref(s)) == status
+    assert lib.cowa_last_error()
+    out = (abi.cowa_window * 4)()
+    assert lib.cowa_windows(ctypes.byref(p), out) == status
+
+
+def _sized(p):
+    s = abi.cowa_schedule_size(p)
+    s.buf = 1 << 20  # a fake, aligned address: these calls must fail before any launch
+    return s
+
+
+def test_fwd_argument_errors_on_host():
+    lib = _lib()
+    p = _good()
+    s = _sized(p)
+    ok = 1 << 24
+    vp = ctypes.c_void_p
+    call = lambda *a: lib.cowa_fwd(ctypes.byref(p), ctypes.byref(s), *[vp(x) for x in a])
+    assert call(0, ok, ok, ok, ok, 0) == abi.COWA_ERR_INVALID_ARG            # q NULL
+    assert call(ok + 8, ok, ok, ok, ok, 0) == abi.COWA_ERR_INVALID_ARG       # q misaligned
+    assert call(ok, ok, ok, ok, ok + 2, 0) == abi.COWA_ERR_INVALID_ARG       # lse misaligned
+    other = _good()
+    other.w_near = 33
+    assert lib.cowa_fwd(ctypes.byref(other), ctypes.byref(s), *[vp(ok)] * 5, vp(0)) == \
+        abi.COWA_ERR_SCHEDULE_MISMATCH
+    s.buf = 4096 + 16
+    assert call(ok, ok, ok, ok, ok, 0) == abi.COWA_ERR_INVALID_ARG           # schedule buffer misaligned
+    s.buf = 0
+    assert call(ok, ok, ok, ok, ok, 0) == abi.COWA_ERR_INVALID_ARG           # schedule buffer NULL
+    # bf16 with a 32-row query block is not built
+    p32 = _good()
+    p32.tile_q = 32
+    s32 = _sized(p32)
+    assert lib.cowa_fwd(ctypes.byref(p32), ctypes.byref(s32), *[vp(ok)] * 5, vp(0)) == abi.COWA_ERR_UNSUPPORTED
+
+
+def test_batch_zero_is_a_no_op():
+    lib = _lib()
+    p = _good()
+    p.batch = 0
+    s = _sized(p)
+    assert lib.cowa_fwd(ctypes.byref(p), ctypes.byref(s), *[ctypes.c_void_p(0)] * 6) == abi.COWA_OK
+
+
+def test_schedule_fields_must_come_from_sizing():
+    lib = _lib()
+    p = _good()
+    s = _sized(p)
+    s.nnz += 1
+    assert lib.cowa_schedule(ctypes.byref(s), None) == abi.COWA_ERR_SCHEDULE_MISMATCH
+
+
+def test_bwd_workspace_and_errors_on_host():
+    lib = _lib()
+    p = _good()
+    need = abi.cowa_bwd_workspace_size(p)
+    rows = p.batch * p.h_q * p.n_q
+    assert need >= rows * p.head_dim * 4 + rows * 4
+    p32 = _good()
+    p32.dtype = abi.COWA_FP32
+    s = _sized(p32)
+    vp = ctypes.c_void_p
+    assert lib.cowa_bwd(ctypes.byref(p32), ctypes.byref(s), *[vp(1 << 24)] * 10, ctypes.c_size_t(need),
+                        vp(0)) == abi.COWA_ERR_UNSUPPORTED
+
+
+def test_decode_argument_errors_on_host():
+    lib = _lib()
+    d = cowa.make_decode_params(4, 8, 2, 128, 1000, 16, 64)
+    need = abi.cowa_decode_workspace_size(d)
+    vp = ctypes.c_void_p
+    ok = 1 << 24
+    assert lib.cowa_decode(ctypes.byref(d), vp(0), vp(ok), vp(ok), vp(ok), vp(ok), vp(ok), vp(ok),
+                           ctypes.c_size_t(need), vp(0)) == abi.COWA_ERR_INVALID_ARG
+    if need > 0:
+        assert lib.cowa_decode(ctypes.byref(d), *[vp(ok)] * 7, ctypes.c_size_t(need - 1), vp(0)) == \
+            abi.COWA_ERR_WORKSPACE
+    bad = cowa.make_decode_params(4, 8, 3, 128, 1000, 16, 64)
+    n = ctypes.c_size_t()
+    assert lib.cowa_decode_workspace_size(ctypes.byref(bad), ctypes.byref(n)) == abi.COWA_ERR_INVALID_ARG
+    bad = cowa.make_decode_params(4, 8, 2, 128, 1000, 16, 64, split_keys=100)
+    assert lib.cowa_decode_workspace_size(ctypes.byref(bad), ctypes.byref(n)) == abi.COWA_ERR_INVALID_ARG

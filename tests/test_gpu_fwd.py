@@ -1,0 +1,115 @@
+"""Forward parity (cowa_fwd through the C ABI) against the fp64 oracle.
+
+Full outputs at the fp32 512-token and the bf16 8K workloads and at odd
+shapes; sampled QO blocks (every row of each sampled block, every QO head) at
+the bf16 32K and 128K workloads, in the launch configuration the benchmark
+times.  Outputs are poisoned with NaN before each call so unwritten elements
+fail.
+"""
+
+import numpy as np
+import pytest
+
+import inputs
+from oracle import attention as ref
+from gpu_util import need_gpu, log, to_dev, to_host, compare, torch
+
+pytestmark = pytest.mark.gpu
+
+
+def _run_fwd(w, t, dev, tile_q=None, tile_k=None):
+    import paper_2609_32704_amd as cowa
+    q, k, v = (to_dev(t[n][0], dev) for n in ("q", "k", "v"))
+    o = torch.full_like(q, float("nan"))
+    lse = torch.full((w.batch, w.h_q, w.n_q), float("nan"), dtype=torch.float32, device=dev)
+    cowa.fwd(q, k, v, w.w_sink, w.w_near, tile_q or w.tile, tile_k or w.tile, w.scale,
+             h_k_total=w.kv_total, h_k_offset=w.h_offset, out=o, lse=lse)
+    torch.cuda.synchronize()
+    return o, lse
+
+
+def _full_check(w, key=None, tile_q=None, tile_k=None):
+    dev = need_gpu()
+    log(f"fwd {w.name}: B={w.batch} n_q={w.n_q} n_k={w.n_k} h={w.h_q}/{w.h_k} d={w.head_dim} "
+        f"sink={w.w_sink} near={w.w_near} tiles={tile_q or w.tile}x{tile_k or w.tile} {w.dtype}")
+    t = inputs.train_tensors(w, which=("q", "k", "v"), key=key)
+    o, lse = _run_fwd(w, t, dev, tile_q, tile_k)
+    o_r, l_r = ref.forward(t["q"][1], t["k"][1], t["v"][1], w.w_sink, w.w_near, w.scale,
+                           h_total=w.kv_total, h_offset=w.h_offset)
+    compare("O", to_host(o), o_r, w.dtype)
+    compare("LSE", to_host(lse), l_r, w.dtype)
+
+
+def test_fwd_fp32_t512():
+    _full_check(inputs.WORKLOADS["fwd_fp32_t512"])
+
+
+def test_fwd_bf16_t8k():
+    _full_check(inputs.WORKLOADS["bf16_t8k"])
+
+
+ODD = [
+    # name, batch, n_q, n_k, h_q, h_k, d, sink, near, tile_q, tile_k, dtype, h_total, h_offset
+    ("tiny", 1, 1, 1, 1, 1, 64, 0, 1, 64, 64, "bf16", 0, 0),
+    ("ragged", 2, 333, 333, 4, 2, 128, 5, 40, 64, 64, "bf16", 0, 0),
+    ("chunked_prefill", 1, 200, 1111, 8, 2, 128, 16, 100, 128, 128, "bf16", 0, 0),
+    ("gqa8", 1, 1000, 1000, 8, 1, 64, 3, 77, 128, 64, "bf16", 0, 0),
+    ("mha", 1, 700, 700, 3, 3, 128, 0, 50, 64, 32, "bf16", 0, 0),
+    ("tp_rank", 1, 2048, 2048, 4, 1, 128, 32, 256, 128, 128, "bf16", 8, 5),
+    ("dense", 1, 777, 777, 4, 2, 128, 0, 777, 128, 128, "bf16", 0, 0),
+    ("wide_windows", 1, 500, 500, 2, 2, 64, 400, 400, 64, 128, "bf16", 0, 0),
+    ("no_near", 1, 300, 300, 2, 2, 64, 0, 0, 64, 64, "bf16", 0, 0),
+    ("fp32_ragged", 1, 301, 450, 4, 2, 128, 7, 33, 64, 32, "fp32", 0, 0),
+    ("fp32_d64", 2, 129, 129, 2, 1, 64, 2, 17, 128, 128, "fp32", 0, 0),
+    ("fp32_tp", 1, 512, 512, 4, 2, 64, 16, 64, 32, 32, "fp32", 4, 2),
+]
+
+
+@pytest.mark.parametrize("case", ODD, ids=[c[0] for c in ODD])
+def test_fwd_odd_shapes(case):
+    name, bsz, n_q, n_k, h_q, h_k, d, ws, wn, tq, tk, dt, ht, ho = case
+    w = inputs.custom("fwd_" + name, batch=bsz, n_q=n_q, n_k=n_k, h_q=h_q, h_k=h_k, head_dim=d, w_sink=ws,
+                      w_near=wn, tile=tq, dtype=dt, h_total=ht, h_offset=ho)
+    _full_check(w, key=inputs.key_of("fwd", name), tile_q=tq, tile_k=tk)
+
+
+def _sampled_check(name, n_blocks, seed):
+    dev = need_gpu()
+    w = inputs.WORKLOADS[name]
+    log(f"fwd {name} sampled: generating inputs")
+    t = inputs.train_tensors(w, which=("q", "k", "v"))
+    o, lse = _run_fwd(w, t, dev)
+    n_qt = -(-w.n_q // w.tile)
+    rng = np.random.default_rng(seed)
+    blocks = sorted(set([0, n_qt - 1] + list(rng.choice(n_qt, size=n_blocks, replace=False))))
+    o_h = o.view(w.batch, w.h_q, w.n_q, w.head_dim)
+    for blk in blocks:
+        b = int(rng.integers(0, w.batch))
+        rows = [(b, h, i) for h in range(w.h_q) for i in range(blk * w.tile, min((blk + 1) * w.tile, w.n_q))]
+        o_r, l_r = ref.forward_rows(t["q"][1], t["k"][1], t["v"][1], rows, w.w_sink, w.w_near, w.scale)
+        sl = slice(blk * w.tile, min((blk + 1) * w.tile, w.n_q))
+        got_o = to_host(o_h[b, :, sl]).reshape(-1, w.head_dim)
+        got_l = lse[b, :, sl].cpu().numpy().astype(np.float64).reshape(-1)
+        log(f" block {blk} (batch {b})")
+        compare("O", got_o, o_r)
+        compare("LSE", got_l, l_r)
+    # no element left unwritten anywhere
+    assert not torch.isnan(o).any().item() and not torch.isnan(lse).any().item()
+
+
+def test_fwd_bf16_t32k_sampled():
+    _sampled_check("bf16_t32k_b2", 6, 1)
+
+
+def test_fwd_bf16_t128k_sampled():
+    _sampled_check("bf16_t128k", 6, 2)
+
+
+def test_fwd_deterministic():
+    dev = need_gpu()
+    w = inputs.custom("fwd_det", batch=1, n_q=2000, n_k=2000, h_q=8, h_k=2, head_dim=128, w_sink=16, w_near=256,
+                      tile=128)
+    t = inputs.train_tensors(w, which=("q", "k", "v"), key=inputs.key_of("det"))
+    o1, l1 = _run_fwd(w, t, dev)
+    o2, l2 = _run_fwd(w, t, dev)
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
