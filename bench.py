@@ -1,0 +1,319 @@
+#!/usr/bin/env python3
+"""Benchmark of the CoWA hot path on one MI355X.
+
+One step is one pass of the whole hot path over one batch of synthetic input:
+
+  window tuples (host) -> schedule build -> forward -> backward (prepare, main,
+  finish) at 131072 tokens, bf16, B=1, H_q=32, H_k=8, d=128, sink 128, near
+  4096, 128x128 blocks; then one decoding step over 64 sequences x 131072
+  cached tokens with the same heads and windows.
+
+``value`` is the effective TFLOP/s of the training path (forward + backward):
+algorithmic FLOPs (4d per legal query-key pair forward, 10d backward, summed
+over every QO head) divided by the mean time of schedule + forward + backward
+per step.  Every kernel is timed with HIP events on the stream it runs on.
+The decoding step is reported as ms and effective HBM GB/s (visible K/V rows,
+q, O and LSE bytes).  Inputs are N(0, 1) bf16 drawn on the device from a
+generator seeded with 42, resident in HBM before timing starts.
+
+Extra blocks in the JSON line:
+  roofline      the dominant kernel (backward main pass) against the bf16
+                MFMA peak; traffic from committed rocprofv3 counter summaries
+  kernels       every kernel's time, work and roofline fraction
+  dense         the same kernels in dense causal mode (w_sink = 0,
+                w_near = N), the in-house FullAttn twin, and CoWA/dense ratios
+  cpu_baseline  the fp64 CPU oracle timed on a bounded sample of the same
+                workload on this host
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
+PAPER_RATIOS = {"fwd": 7.4, "bwd": 8.6, "decode": 3.0,
+                "hardware": "8x NVIDIA H100 (SM90), TP=8, BF16, batch 1, 64 QO / 8 KV heads, d=128, 128K"}
+
+TRAIN = dict(batch=1, n=131072, h_q=32, h_k=8, d=128, w_sink=128, w_near=4096, tile=128)
+DECODE = dict(batch=64, n=131072, h_q=32, h_k=8, d=128, w_sink=128, w_near=4096)
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def source_digest(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def read_traffic(kernel):
+    """HBM bytes per launch from the committed counter summary
+    (profiles/hbm_traffic.txt), or None when missing or when the kernel's
+    source changed after the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        parts = line.split()
+        if len(parts) >= 4 and parts[0] == kernel and not line.startswith("#"):
+            src, digest, nbytes = parts[1], parts[2], parts[3]
+            try:
+                if source_digest(os.path.join(ROOT, src)) != digest:
+                    return None
+            except OSError:
+                return None
+            return float(nbytes)
+    return None
+
+
+def cpu_baseline(target_s=12.0):
+    """The fp64 oracle (as it stands) on a bounded sample of the 128K training
+    workload: every QO-head row of a few 128-row query blocks, full forward
+    and backward work of those rows (their dK/dV contributions included)."""
+    import numpy as np
+    import inputs
+    from oracle import attention as ref, counts
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [os.cpu_count() or 1])
+    except Exception:  # noqa: BLE001
+        threads = os.cpu_count() or 1
+    w = inputs.WORKLOADS["bf16_t128k"]
+    rng = np.random.default_rng(7)
+    # inputs: the rows the sample touches come from the same seeded streams (full tensors)
+    log("cpu_baseline: generating inputs")
+    t = inputs.train_tensors(w)
+    q, k, v, do = (t[n][1] for n in ("q", "k", "v", "do"))
+    sizes = {hk: counts.support_table(w.n_q, w.n_k, w.w_sink, w.w_near, w.h_k)[hk] for hk in range(w.h_k)}
+    done_pairs, elapsed, blocks = 0, 0.0, []
+    n_qt = w.n_q // w.tile
+    while elapsed < target_s and len(blocks) < 64:
+        blk = int(rng.integers(0, n_qt))
+        h = int(rng.integers(0, w.h_q))
+        rows = np.arange(blk * w.tile, (blk + 1) * w.tile)
+        t0 = time.perf_counter()
+        ref.backward(q, k, v, do, w.w_sink, w.w_near, w.scale, rows=rows, heads=[h])
+        elapsed += time.perf_counter() - t0
+        done_pairs += int(sizes[(h * w.h_k) // w.h_q][rows].sum())
+        blocks.append((h, blk))
+    flops = 14 * w.head_dim * done_pairs
+    return {"value": flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "seconds": round(elapsed, 3),
+            "sample": f"{len(blocks)} (QO head, 128-row query block) pairs of the 131072-token workload, "
+                      f"full fp64 forward+backward of those rows ({done_pairs} legal pairs, 14d FLOPs each)"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--dense-iters", type=int, default=2)
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on exactly one GPU: the CoWA path shards by KV head with no exchange, "
+              "and this build measures one device's share (--gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_32704_amd as cowa
+    from paper_2609_32704_amd import _abi
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream().cuda_stream
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(42)
+
+    def randn(shape):
+        """N(0, 1) bf16 drawn on the device, one leading slice at a time."""
+        out = torch.empty(shape, dtype=torch.bfloat16, device=dev)
+        for s in range(shape[0]):
+            out[s].copy_(torch.randn(shape[1:], generator=gen, device=dev, dtype=torch.float32))
+        return out
+
+    T = TRAIN
+    log("allocating training inputs")
+    q = randn((T["batch"], T["h_q"], T["n"], T["d"]))
+    k = randn((T["batch"], T["h_k"], T["n"], T["d"]))
+    v = randn((T["batch"], T["h_k"], T["n"], T["d"]))
+    do = randn((T["batch"], T["h_q"], T["n"], T["d"]))
+    o = torch.empty_like(q)
+    lse = torch.empty((T["batch"], T["h_q"], T["n"]), dtype=torch.float32, device=dev)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+
+    def params(w_sink, w_near):
+        return cowa.make_params(T["batch"], T["n"], T["n"], T["h_q"], T["h_k"], T["d"], w_sink, w_near,
+                                T["tile"], T["tile"])
+
+    p = params(T["w_sink"], T["w_near"])
+    sched = cowa.Schedule(p, dev, build=False)
+    ws_bytes = _abi.cowa_bwd_workspace_size(p)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    pairs = _abi.cowa_legal_pairs(p)
+    fwd_flops = 4 * T["d"] * pairs
+    bwd_flops = 10 * T["d"] * pairs
+
+    D = DECODE
+    log("allocating decode inputs (2 x 17 GB KV cache)")
+    dq_in = randn((D["batch"], D["h_q"], D["d"]))
+    kc = randn((D["batch"], D["h_k"], D["n"], D["d"]))
+    vc = randn((D["batch"], D["h_k"], D["n"], D["d"]))
+    seqlens_host = [D["n"]] * D["batch"]
+    seqlens = torch.tensor(seqlens_host, dtype=torch.int32, device=dev)
+    dpar = cowa.make_decode_params(D["batch"], D["h_q"], D["h_k"], D["d"], D["n"], D["w_sink"], D["w_near"])
+    dws = torch.empty(_abi.cowa_decode_workspace_size(dpar), dtype=torch.uint8, device=dev)
+    od = torch.empty_like(dq_in)
+    lsed = torch.empty((D["batch"], D["h_q"]), dtype=torch.float32, device=dev)
+    vis_keys = _abi.cowa_decode_visible_keys(dpar, seqlens_host)
+    dec_bytes = 2 * vis_keys * D["d"] * 2 + D["batch"] * D["h_q"] * (2 * D["d"] * 2 + 4)
+
+    names = ["schedule", "fwd", "bwd_prepare", "bwd_main", "bwd_finish", "decode"]
+
+    def step(evs):
+        evs[0].record()
+        _abi.cowa_windows(p)
+        _abi.cowa_schedule(sched.s, stream)
+        evs[1].record()
+        _abi.cowa_fwd(p, sched.s, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), stream)
+        evs[2].record()
+        _abi.cowa_bwd_prepare(p, o.data_ptr(), do.data_ptr(), ws.data_ptr(), ws_bytes, stream)
+        evs[3].record()
+        _abi.cowa_bwd_main(p, sched.s, q.data_ptr(), k.data_ptr(), v.data_ptr(), lse.data_ptr(), do.data_ptr(),
+                           dk.data_ptr(), dv.data_ptr(), ws.data_ptr(), ws_bytes, stream)
+        evs[4].record()
+        _abi.cowa_bwd_finish(p, dq.data_ptr(), ws.data_ptr(), ws_bytes, stream)
+        evs[5].record()
+        _abi.cowa_decode(dpar, dq_in.data_ptr(), kc.data_ptr(), vc.data_ptr(), seqlens.data_ptr(), od.data_ptr(),
+                         lsed.data_ptr(), dws.data_ptr(), dws.numel(), stream)
+        evs[6].record()
+
+    def new_events():
+        return [torch.cuda.Event(enable_timing=True) for _ in range(7)]
+
+    log(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        step(new_events())
+    torch.cuda.synchronize()
+    log(f"timing {args.steps} steps")
+    all_evs = [new_events() for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for evs in all_evs:
+        step(evs)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = {n: 0.0 for n in names}
+    for evs in all_evs:
+        for idx, n in enumerate(names):
+            per[n] += evs[idx].elapsed_time(evs[idx + 1])
+    per = {n: per[n] / args.steps for n in names}
+    bwd_ms = per["bwd_prepare"] + per["bwd_main"] + per["bwd_finish"]
+    train_ms = per["schedule"] + per["fwd"] + bwd_ms
+    value = (fwd_flops + bwd_flops) / (train_ms * 1e-3) / 1e12
+
+    rows_q = T["batch"] * T["h_q"] * T["n"]
+    elem_q = rows_q * T["d"]
+    kernels = {
+        "schedule": {"ms": per["schedule"], "bound": "launch", "note": "three small kernels"},
+        "fwd": {"ms": per["fwd"], "bound": "mfma", "work": fwd_flops, "unit": "TFLOP/s",
+                "achieved": fwd_flops / (per["fwd"] * 1e-3) / 1e12},
+        "bwd_prepare": {"ms": per["bwd_prepare"], "bound": "hbm", "unit": "GB/s",
+                        "work": 2 * elem_q * 2 + rows_q * 4 + elem_q * 4,
+                        "achieved": (2 * elem_q * 2 + rows_q * 4 + elem_q * 4) / (per["bwd_prepare"] * 1e-3) / 1e9},
+        "bwd_main": {"ms": per["bwd_main"], "bound": "mfma", "work": bwd_flops, "unit": "TFLOP/s",
+                     "achieved": bwd_flops / (per["bwd_main"] * 1e-3) / 1e12},
+        "bwd_finish": {"ms": per["bwd_finish"], "bound": "hbm", "unit": "GB/s", "work": elem_q * 4 + elem_q * 2,
+                       "achieved": (elem_q * 6) / (per["bwd_finish"] * 1e-3) / 1e9},
+        "decode": {"ms": per["decode"], "bound": "hbm", "unit": "GB/s", "work": dec_bytes,
+                   "achieved": dec_bytes / (per["decode"] * 1e-3) / 1e9},
+    }
+    for kn in kernels.values():
+        if kn["bound"] == "mfma":
+            kn["frac"] = kn["achieved"] / PEAK_BF16_TFLOPS
+        elif kn["bound"] == "hbm":
+            kn["frac"] = kn["achieved"] / PEAK_HBM_GBPS
+
+    main_k = kernels["bwd_main"]
+    traffic = read_traffic("bwd_main")
+    roofline = {"kernel": "bwd_main (backward main pass, 131072 tokens)", "bound": "mfma",
+                "achieved": main_k["achieved"], "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": main_k["frac"], "traffic": traffic,
+                "work_per_launch": f"{bwd_flops:.4e} FLOP = 10 d x {pairs} legal pairs"}
+
+    dense = None
+    if not args.no_dense and args.dense_iters > 0:
+        log("dense causal twin")
+        pd = params(0, T["n"])
+        sd = cowa.Schedule(pd, dev)
+        dpairs = _abi.cowa_legal_pairs(pd)
+        ddp = cowa.make_decode_params(D["batch"], D["h_q"], D["h_k"], D["d"], D["n"], 0, D["n"])
+        dws2 = torch.empty(_abi.cowa_decode_workspace_size(ddp), dtype=torch.uint8, device=dev)
+        times = {"fwd": 0.0, "bwd": 0.0, "decode": 0.0}
+        for it in range(args.dense_iters + 1):
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+            e[0].record()
+            _abi.cowa_fwd(pd, sd.s, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), stream)
+            e[1].record()
+            _abi.cowa_bwd(pd, sd.s, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
+                          do.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), ws.data_ptr(), ws_bytes,
+                          stream)
+            e[2].record()
+            _abi.cowa_decode(ddp, dq_in.data_ptr(), kc.data_ptr(), vc.data_ptr(), seqlens.data_ptr(),
+                             od.data_ptr(), lsed.data_ptr(), dws2.data_ptr(), dws2.numel(), stream)
+            e[3].record()
+            torch.cuda.synchronize()
+            if it > 0:
+                times["fwd"] += e[0].elapsed_time(e[1])
+                times["bwd"] += e[1].elapsed_time(e[2])
+                times["decode"] += e[2].elapsed_time(e[3])
+        times = {kk: vv / args.dense_iters for kk, vv in times.items()}
+        cowa_fwd_ms = per["schedule"] + per["fwd"]
+        dense = {"fwd_ms": times["fwd"], "bwd_ms": times["bwd"], "decode_ms": times["decode"],
+                 "fwd_tflops": 4 * T["d"] * dpairs / (times["fwd"] * 1e-3) / 1e12,
+                 "bwd_tflops": 10 * T["d"] * dpairs / (times["bwd"] * 1e-3) / 1e12,
+                 "ratio_fwd": times["fwd"] / cowa_fwd_ms, "ratio_bwd": times["bwd"] / bwd_ms,
+                 "ratio_decode": times["decode"] / per["decode"],
+                 "work_ratio_train": dpairs / pairs,
+                 "paper_ratios": PAPER_RATIOS, "iters": args.dense_iters}
+
+    cpu = None
+    if not args.no_cpu:
+        log("cpu baseline (fp64 oracle on a bounded sample)")
+        cpu = cpu_baseline()
+
+    out = {
+        "metric": "fwd/bwd ms + effective TFLOP/s at 128K bf16; decode ms/step and HBM GB/s",
+        "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "CoWA fwd+bwd at 131072 tokens + decode of 64 x 131072-token caches",
+                   "batch": T["batch"], "seq_len": T["n"], "h_q": T["h_q"], "h_k": T["h_k"],
+                   "head_dim": T["d"], "w_sink": T["w_sink"], "w_near": T["w_near"], "tile": T["tile"],
+                   "decode_batch": D["batch"], "decode_cache_len": D["n"],
+                   "parallelism": "one GPU holding all 8 KV heads (the 8 KV-head TP shares)"},
+        "fwd_ms": per["schedule"] + per["fwd"], "bwd_ms": bwd_ms,
+        "fwd_tflops": fwd_flops / ((per["schedule"] + per["fwd"]) * 1e-3) / 1e12,
+        "bwd_tflops": bwd_flops / (bwd_ms * 1e-3) / 1e12,
+        "decode_ms": per["decode"], "decode_gbps": dec_bytes / (per["decode"] * 1e-3) / 1e9,
+        "legal_pairs": pairs, "decode_visible_keys": vis_keys,
+        "roofline": roofline, "kernels": kernels, "dense": dense, "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

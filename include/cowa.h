@@ -124,6 +124,16 @@ cowa_status cowa_windows(const cowa_params* p, cowa_window* out_host);
  * I_h(j)): fills every field of *out except buf.  Host only, O(h_k (n_qt + n_kt)). */
 cowa_status cowa_schedule_size(const cowa_params* p, cowa_schedule_t* out);
 
+/* Work accounting (host only): the number of legal (query, key) pairs of
+ * Eq. fwa_support summed over the batch and every QO head.  Attention FLOPs
+ * follow from it (App. A.2 and A.3: 4d per pair forward, 10d backward). */
+cowa_status cowa_legal_pairs(const cowa_params* p, int64_t* pairs);
+
+/* Work accounting of one decoding step (host only): visible keys summed over
+ * the sequences (seqlens_host: host int32 [batch]) and the local KV heads;
+ * each is one K row and one V row read.  Invalid lengths count zero. */
+cowa_status cowa_decode_visible_keys(const cowa_decode_params* p, const int32_t* seqlens_host, int64_t* keys);
+
 /* Build the schedule into s->buf on the device (three small kernels:
  * per-row counts, prefix sums, entry fill). */
 cowa_status cowa_schedule(const cowa_schedule_t* s, void* stream);
@@ -142,12 +152,33 @@ cowa_status cowa_bwd_workspace_size(const cowa_params* p, size_t* bytes);
 
 /* Backward (Alg. 2): exact gradients of <dO, O> w.r.t. the unscaled Q, K and
  * V, using the saved O and LSE of the forward.  dq like q; dk/dv like k/v
- * (keys that no query sees get zero).  bf16 only. */
+ * (keys that no query sees get zero).  bf16 only; tile_q and tile_k in
+ * {64, 128}.  Equivalent to cowa_bwd_prepare, cowa_bwd_main and
+ * cowa_bwd_finish in that order on the same workspace. */
 cowa_status cowa_bwd(const cowa_params* p, const cowa_schedule_t* s,
                      const void* q, const void* k, const void* v,
                      const void* o, const float* lse, const void* d_o,
                      void* dq, void* dk, void* dv,
                      void* workspace, size_t ws_bytes, void* stream);
+
+/* Backward stage 1: the row sums D = rowsum(O * dO) of Alg. 2 (the term
+ * subtracted from dP) into the workspace, and the workspace's float32 dQ
+ * accumulator set to zero. */
+cowa_status cowa_bwd_prepare(const cowa_params* p, const void* o, const void* d_o,
+                             void* workspace, size_t ws_bytes, void* stream);
+
+/* Backward stage 2 (the loop of Alg. 2): for every local KV head and KV block,
+ * over every QO head of its group and every QO block of I_h(j) in ascending
+ * order, recompute P from LSE, form dS, accumulate dK and dV of the block
+ * (written once, no atomics) and add dS K into the dQ accumulator (float32
+ * atomics).  Needs the workspace filled by cowa_bwd_prepare. */
+cowa_status cowa_bwd_main(const cowa_params* p, const cowa_schedule_t* s,
+                          const void* q, const void* k, const void* v,
+                          const float* lse, const void* d_o, void* dk, void* dv,
+                          void* workspace, size_t ws_bytes, void* stream);
+
+/* Backward stage 3: dq = bfloat16(dQ accumulator). */
+cowa_status cowa_bwd_finish(const cowa_params* p, void* dq, void* workspace, size_t ws_bytes, void* stream);
 
 /* Workspace bytes of one decoding step: split partial states (m, l, O). */
 cowa_status cowa_decode_workspace_size(const cowa_decode_params* p, size_t* bytes);

@@ -134,8 +134,11 @@ def forward_rows(q, k, v, rows, w_sink, w_near, scale, h_total=None, h_offset=0,
     return out_o, out_l
 
 
-def backward(q, k, v, do, w_sink, w_near, scale, h_total=None, h_offset=0, block=256):
-    """Exact gradient of <dO, O(Q, K, V)>.  Returns (dQ, dK, dV, O, LSE)."""
+def backward(q, k, v, do, w_sink, w_near, scale, h_total=None, h_offset=0, block=256, rows=None, heads=None):
+    """Exact gradient of <dO, O(Q, K, V)>.  Returns (dQ, dK, dV, O, LSE).
+
+    ``rows`` / ``heads`` restrict the work to those query rows and QO heads
+    (default: all); dK and dV then hold only their contributions."""
     q, k, v, do = (np.asarray(x, dtype=np.float64) for x in (q, k, v, do))
     bsz, h_q, n_q, d = q.shape
     h_k, n_k = k.shape[1], k.shape[2]
@@ -145,10 +148,11 @@ def backward(q, k, v, do, w_sink, w_near, scale, h_total=None, h_offset=0, block
     dv = np.zeros_like(v)
     o = np.zeros_like(do)
     lse = np.zeros((bsz, h_q, n_q))
+    row_set = np.arange(n_q) if rows is None else np.asarray(rows, dtype=np.int64)
     for b in range(bsz):
-        for h in range(h_q):
+        for h in (range(h_q) if heads is None else heads):
             hk = kv_head_of(h, h_q, h_k)
-            for rows in _blocks(np.arange(n_q), block):
+            for rows in _blocks(row_set, block):
                 ob, lb, keys, p = _rows_forward(q[b, h], k[b, hk], v[b, hk], rows, n_q, n_k,
                                                 w_sink, w_near, h_offset + hk, h_total, scale)
                 o[b, h, rows] = ob
@@ -210,9 +214,10 @@ def backward_kv_rows(q, k, v, do, kv_rows, w_sink, w_near, scale, h_total=None, 
     return out_dk, out_dv
 
 
-def backward_q_rows(q, k, v, do, rows, w_sink, w_near, scale, h_total=None, h_offset=0):
-    """Exact dQ (and O, LSE) of selected query rows ``(b, h, i_q)``.
-    Returns (dq [n, d], o [n, d], lse [n])."""
+def backward_q_rows(q, k, v, do, rows, w_sink, w_near, scale, h_total=None, h_offset=0, block=128):
+    """Exact dQ (and O, LSE) of selected query rows ``(b, h, i_q)``, evaluated in
+    blocks of nearby rows of one (batch, QO head).
+    Returns (dq [n, d], o [n, d], lse [n]) in the order given."""
     q, k, v, do = (np.asarray(x, dtype=np.float64) for x in (q, k, v, do))
     h_q, n_q = q.shape[1], q.shape[2]
     h_k, n_k = k.shape[1], k.shape[2]
@@ -221,18 +226,25 @@ def backward_q_rows(q, k, v, do, rows, w_sink, w_near, scale, h_total=None, h_of
     out_dq = np.zeros((len(rows), q.shape[3]))
     out_o = np.zeros((len(rows), v.shape[3]))
     out_l = np.zeros(len(rows))
+    groups = {}
     for n, (b, h, i) in enumerate(rows):
+        groups.setdefault((b, h), []).append((i, n))
+    for (b, h), lst in groups.items():
+        lst.sort()
         hk = kv_head_of(h, h_q, h_k)
-        idx = np.array([i], dtype=np.int64)
-        ob, lb, keys, p = _rows_forward(q[b, h], k[b, hk], v[b, hk], idx, n_q, n_k,
-                                        w_sink, w_near, h_offset + hk, h_total, scale)
-        out_o[n], out_l[n] = ob[0], lb[0]
-        if keys.size == 0:
-            continue
-        dp = do[b, h, idx] @ v[b, hk, keys].T
-        dsum = (ob * do[b, h, idx]).sum(axis=1)
-        ds = p * (dp - dsum[:, None])
-        out_dq[n] = scale * (ds @ k[b, hk, keys])[0]
+        for s in range(0, len(lst), block):
+            chunk = lst[s:s + block]
+            idx = np.array([i for i, _ in chunk], dtype=np.int64)
+            ob, lb, keys, p = _rows_forward(q[b, h], k[b, hk], v[b, hk], idx, n_q, n_k,
+                                            w_sink, w_near, h_offset + hk, h_total, scale)
+            dqb = np.zeros((len(idx), q.shape[3]))
+            if keys.size:
+                dp = do[b, h, idx] @ v[b, hk, keys].T
+                dsum = (ob * do[b, h, idx]).sum(axis=1)
+                ds = p * (dp - dsum[:, None])
+                dqb = scale * (ds @ k[b, hk, keys])
+            for t, (_, n) in enumerate(chunk):
+                out_dq[n], out_o[n], out_l[n] = dqb[t], ob[t], lb[t]
     return out_dq, out_o, out_l
 
 

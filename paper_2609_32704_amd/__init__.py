@@ -143,7 +143,7 @@ def fwd(q, k, v, w_sink, w_near, tile_q, tile_k, softmax_scale=None, h_k_total=N
 
 
 def bwd(q, k, v, o, lse, do, w_sink, w_near, tile_q, tile_k, softmax_scale=None, h_k_total=None, h_k_offset=0,
-        schedule=None, workspace=None, stream=None):
+        schedule=None, workspace=None, dq=None, dk=None, dv=None, stream=None):
     """cowa_bwd.  Returns (dq, dk, dv) for bf16 inputs."""
     torch = _torch()
     for t, n in ((q, "q"), (o, "o"), (do, "do")):
@@ -160,9 +160,12 @@ def bwd(q, k, v, o, lse, do, w_sink, w_near, tile_q, tile_k, softmax_scale=None,
     need = _abi.cowa_bwd_workspace_size(p)
     if workspace is None:
         workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=q.device)
-    dq = torch.empty_like(q)
-    dk = torch.empty_like(k)
-    dv = torch.empty_like(v)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    _check(dq, "dq", q.dtype, 4)
+    _check(dk, "dk", q.dtype, 4)
+    _check(dv, "dv", q.dtype, 4)
     _abi.cowa_bwd(p, schedule.s, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
                   do.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), workspace.data_ptr(),
                   workspace.numel(), _stream(stream))

@@ -61,10 +61,16 @@ _SIGNATURES = {
     "cowa_windows": (ctypes.c_int, [_P(cowa_params), _P(cowa_window)]),
     "cowa_schedule_size": (ctypes.c_int, [_P(cowa_params), _P(cowa_schedule_t)]),
     "cowa_schedule": (ctypes.c_int, [_P(cowa_schedule_t), _vp]),
+    "cowa_legal_pairs": (ctypes.c_int, [_P(cowa_params), _P(ctypes.c_int64)]),
+    "cowa_decode_visible_keys": (ctypes.c_int, [_P(cowa_decode_params), _P(ctypes.c_int32), _P(ctypes.c_int64)]),
     "cowa_fwd": (ctypes.c_int, [_P(cowa_params), _P(cowa_schedule_t), _vp, _vp, _vp, _vp, _vp, _vp]),
     "cowa_bwd_workspace_size": (ctypes.c_int, [_P(cowa_params), _P(ctypes.c_size_t)]),
     "cowa_bwd": (ctypes.c_int, [_P(cowa_params), _P(cowa_schedule_t), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                 _vp, _vp, ctypes.c_size_t, _vp]),
+    "cowa_bwd_prepare": (ctypes.c_int, [_P(cowa_params), _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+    "cowa_bwd_main": (ctypes.c_int, [_P(cowa_params), _P(cowa_schedule_t), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                     ctypes.c_size_t, _vp]),
+    "cowa_bwd_finish": (ctypes.c_int, [_P(cowa_params), _vp, _vp, ctypes.c_size_t, _vp]),
     "cowa_decode_workspace_size": (ctypes.c_int, [_P(cowa_decode_params), _P(ctypes.c_size_t)]),
     "cowa_decode": (ctypes.c_int, [_P(cowa_decode_params), _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t,
                                    _vp]),
@@ -126,6 +132,19 @@ def cowa_schedule(sched, stream):
     check(lib().cowa_schedule(ctypes.byref(sched), _vp(stream)))
 
 
+def cowa_legal_pairs(params):
+    n = ctypes.c_int64()
+    check(lib().cowa_legal_pairs(ctypes.byref(params), ctypes.byref(n)))
+    return n.value
+
+
+def cowa_decode_visible_keys(dparams, seqlens_host):
+    arr = (ctypes.c_int32 * len(seqlens_host))(*[int(x) for x in seqlens_host])
+    n = ctypes.c_int64()
+    check(lib().cowa_decode_visible_keys(ctypes.byref(dparams), arr, ctypes.byref(n)))
+    return n.value
+
+
 def cowa_fwd(params, sched, q, k, v, o, lse, stream):
     check(lib().cowa_fwd(ctypes.byref(params), ctypes.byref(sched), _vp(q), _vp(k), _vp(v), _vp(o), _vp(lse),
                          _vp(stream)))
@@ -140,6 +159,19 @@ def cowa_bwd_workspace_size(params):
 def cowa_bwd(params, sched, q, k, v, o, lse, d_o, dq, dk, dv, workspace, ws_bytes, stream):
     check(lib().cowa_bwd(ctypes.byref(params), ctypes.byref(sched), _vp(q), _vp(k), _vp(v), _vp(o), _vp(lse),
                          _vp(d_o), _vp(dq), _vp(dk), _vp(dv), _vp(workspace), ws_bytes, _vp(stream)))
+
+
+def cowa_bwd_prepare(params, o, d_o, workspace, ws_bytes, stream):
+    check(lib().cowa_bwd_prepare(ctypes.byref(params), _vp(o), _vp(d_o), _vp(workspace), ws_bytes, _vp(stream)))
+
+
+def cowa_bwd_main(params, sched, q, k, v, lse, d_o, dk, dv, workspace, ws_bytes, stream):
+    check(lib().cowa_bwd_main(ctypes.byref(params), ctypes.byref(sched), _vp(q), _vp(k), _vp(v), _vp(lse),
+                              _vp(d_o), _vp(dk), _vp(dv), _vp(workspace), ws_bytes, _vp(stream)))
+
+
+def cowa_bwd_finish(params, dq, workspace, ws_bytes, stream):
+    check(lib().cowa_bwd_finish(ctypes.byref(params), _vp(dq), _vp(workspace), ws_bytes, _vp(stream)))
 
 
 def cowa_decode_workspace_size(dparams):

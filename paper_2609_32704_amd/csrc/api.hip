@@ -172,6 +172,40 @@ cowa_status cowa_schedule_size(const cowa_params* p, cowa_schedule_t* out) {
   return COWA_OK;
 }
 
+cowa_status cowa_legal_pairs(const cowa_params* p, int64_t* pairs) {
+  COWA_TRY(check_params(p));
+  if (!pairs) return fail(COWA_ERR_INVALID_ARG, "pairs is NULL");
+  const int64_t off = (int64_t)p->n_k - p->n_q;
+  int64_t total = 0;
+  for (int h = 0; h < p->h_k; ++h) {
+    int64_t lo, hi;
+    cowa::long_bounds(p->n_k, p->w_sink, p->w_near, (int64_t)p->h_k_offset + h, p->h_k_total, &lo, &hi);
+    for (int64_t iq = 0; iq < p->n_q; ++iq)  // runs of the query whose distance-0 key is iq + off
+      total += cowa::ranges_count(cowa::decode_key_runs(iq + off + 1, p->w_sink, p->w_near, lo, hi));
+  }
+  *pairs = total * (p->h_q / p->h_k) * (int64_t)p->batch;
+  return COWA_OK;
+}
+
+cowa_status cowa_decode_visible_keys(const cowa_decode_params* p, const int32_t* seqlens_host, int64_t* keys) {
+  if (!p || !seqlens_host || !keys) return fail(COWA_ERR_INVALID_ARG, "NULL argument");
+  if (p->batch < 0 || p->h_k < 1 || p->h_k_total < 1 || p->h_k_offset < 0 ||
+      (int64_t)p->h_k_offset + p->h_k > p->h_k_total || p->w_sink < 0 || p->w_near < 0)
+    return fail(COWA_ERR_INVALID_ARG, "invalid decode parameters");
+  int64_t total = 0;
+  for (int b = 0; b < p->batch; ++b) {
+    const int64_t n_k = seqlens_host[b];
+    if (n_k < 1 || n_k > p->n_max) continue;
+    for (int h = 0; h < p->h_k; ++h) {
+      int64_t lo, hi;
+      cowa::long_bounds(n_k, p->w_sink, p->w_near, (int64_t)p->h_k_offset + h, p->h_k_total, &lo, &hi);
+      total += cowa::ranges_count(cowa::decode_key_runs(n_k, p->w_sink, p->w_near, lo, hi));
+    }
+  }
+  *keys = total;
+  return COWA_OK;
+}
+
 cowa_status cowa_schedule(const cowa_schedule_t* s, void* stream) {
   if (!s) return fail(COWA_ERR_INVALID_ARG, "schedule is NULL");
   COWA_TRY(check_params(&s->p));
@@ -218,36 +252,81 @@ cowa_status cowa_bwd_workspace_size(const cowa_params* p, size_t* bytes) {
   return COWA_OK;
 }
 
-cowa_status cowa_bwd(const cowa_params* p, const cowa_schedule_t* s, const void* q, const void* k, const void* v,
-                     const void* o, const float* lse, const void* d_o, void* dq, void* dk, void* dv, void* workspace,
-                     size_t ws_bytes, void* stream) {
+// Common checks of the backward stages; fills the workspace views.
+static cowa_status check_bwd(const cowa_params* p, size_t ws_bytes, void* workspace, float** dq_acc, float** dsum) {
   COWA_TRY(check_params(p));
-  COWA_TRY(check_schedule(p, s));
-  if (p->batch == 0) return COWA_OK;
   if (p->dtype != COWA_BF16) return fail(COWA_ERR_UNSUPPORTED, "backward is built for bf16 only");
   if (!cowa::bwd_bf16_supported(p->head_dim, p->tile_q, p->tile_k))
-    return fail(COWA_ERR_UNSUPPORTED, "bf16 backward is not built for head_dim %d, tiles %d x %d", p->head_dim,
+    return fail(COWA_ERR_UNSUPPORTED, "bf16 backward is built for tile_q, tile_k in {64, 128} (got %d x %d)",
                 p->tile_q, p->tile_k);
+  size_t need = 0;
+  COWA_TRY(cowa_bwd_workspace_size(p, &need));
+  if (p->batch > 0 && (!workspace || ws_bytes < need || !aligned(workspace, 256)))
+    return fail(COWA_ERR_WORKSPACE, "backward needs a 256-byte aligned workspace of %zu bytes (got %zu)", need, ws_bytes);
+  const size_t rows = (size_t)p->batch * p->h_q * p->n_q;
+  *dq_acc = static_cast<float*>(workspace);
+  *dsum = reinterpret_cast<float*>(static_cast<char*>(workspace) + align256(rows * p->head_dim * sizeof(float)));
+  return COWA_OK;
+}
+
+cowa_status cowa_bwd_prepare(const cowa_params* p, const void* o, const void* d_o, void* workspace, size_t ws_bytes,
+                             void* stream) {
+  float *dq_acc, *dsum;
+  COWA_TRY(check_bwd(p, ws_bytes, workspace, &dq_acc, &dsum));
+  if (p->batch == 0) return COWA_OK;
+  COWA_TRY(check_tensor(o, "o", 16));
+  COWA_TRY(check_tensor(d_o, "d_o", 16));
+  COWA_TRY(check_device());
+  return hip_status(cowa::launch_bwd_prepare(*p, o, d_o, dq_acc, dsum, static_cast<hipStream_t>(stream)),
+                    "backward prepare launch");
+}
+
+cowa_status cowa_bwd_main(const cowa_params* p, const cowa_schedule_t* s, const void* q, const void* k,
+                          const void* v, const float* lse, const void* d_o, void* dk, void* dv, void* workspace,
+                          size_t ws_bytes, void* stream) {
+  float *dq_acc, *dsum;
+  COWA_TRY(check_bwd(p, ws_bytes, workspace, &dq_acc, &dsum));
+  COWA_TRY(check_schedule(p, s));
+  if (p->batch == 0) return COWA_OK;
   COWA_TRY(check_tensor(q, "q", 16));
   COWA_TRY(check_tensor(k, "k", 16));
   COWA_TRY(check_tensor(v, "v", 16));
-  COWA_TRY(check_tensor(o, "o", 16));
   COWA_TRY(check_tensor(lse, "lse", 4));
   COWA_TRY(check_tensor(d_o, "d_o", 16));
-  COWA_TRY(check_tensor(dq, "dq", 16));
   COWA_TRY(check_tensor(dk, "dk", 16));
   COWA_TRY(check_tensor(dv, "dv", 16));
-  size_t need = 0;
-  COWA_TRY(cowa_bwd_workspace_size(p, &need));
-  if (!workspace || ws_bytes < need || !aligned(workspace, 256))
-    return fail(COWA_ERR_WORKSPACE, "backward needs a 256-byte aligned workspace of %zu bytes (got %zu)", need, ws_bytes);
+  if ((int64_t)s->n_kt * p->h_k * p->batch >= (int64_t(1) << 31))
+    return fail(COWA_ERR_UNSUPPORTED, "too many key blocks for one launch");
   COWA_TRY(check_device());
-  const size_t rows = (size_t)p->batch * p->h_q * p->n_q;
-  float* dq_acc = static_cast<float*>(workspace);
-  float* dsum = reinterpret_cast<float*>(static_cast<char*>(workspace) + align256(rows * p->head_dim * sizeof(float)));
-  return hip_status(cowa::launch_bwd_bf16(*p, cowa::sched_view(s), q, k, v, o, lse, d_o, dq, dk, dv, dq_acc, dsum,
+  return hip_status(cowa::launch_bwd_main(*p, cowa::sched_view(s), q, k, v, lse, d_o, dk, dv, dq_acc, dsum,
                                           static_cast<hipStream_t>(stream)),
-                    "backward launch");
+                    "backward main launch");
+}
+
+cowa_status cowa_bwd_finish(const cowa_params* p, void* dq, void* workspace, size_t ws_bytes, void* stream) {
+  float *dq_acc, *dsum;
+  COWA_TRY(check_bwd(p, ws_bytes, workspace, &dq_acc, &dsum));
+  if (p->batch == 0) return COWA_OK;
+  COWA_TRY(check_tensor(dq, "dq", 16));
+  COWA_TRY(check_device());
+  return hip_status(cowa::launch_bwd_finish(*p, dq_acc, dq, static_cast<hipStream_t>(stream)),
+                    "backward finish launch");
+}
+
+cowa_status cowa_bwd(const cowa_params* p, const cowa_schedule_t* s, const void* q, const void* k, const void* v,
+                     const void* o, const float* lse, const void* d_o, void* dq, void* dk, void* dv, void* workspace,
+                     size_t ws_bytes, void* stream) {
+  float *dq_acc, *dsum;
+  COWA_TRY(check_bwd(p, ws_bytes, workspace, &dq_acc, &dsum));
+  COWA_TRY(check_schedule(p, s));
+  if (p->batch == 0) return COWA_OK;
+  const void* ptrs[] = {q, k, v, o, d_o, dq, dk, dv};
+  const char* names[] = {"q", "k", "v", "o", "d_o", "dq", "dk", "dv"};
+  for (int x = 0; x < 8; ++x) COWA_TRY(check_tensor(ptrs[x], names[x], 16));
+  COWA_TRY(check_tensor(lse, "lse", 4));
+  COWA_TRY(cowa_bwd_prepare(p, o, d_o, workspace, ws_bytes, stream));
+  COWA_TRY(cowa_bwd_main(p, s, q, k, v, lse, d_o, dk, dv, workspace, ws_bytes, stream));
+  return cowa_bwd_finish(p, dq, workspace, ws_bytes, stream);
 }
 
 static cowa_status check_decode_params(const cowa_decode_params* p) {

@@ -7,8 +7,11 @@ import pytest
 
 torch = pytest.importorskip("torch")
 
-# bf16 outputs: max |x - ref| <= 2e-2 and ||x - ref||_F / ||ref||_F <= 1e-2, per tensor;
-# fp32 outputs: both <= 1e-5.
+# Parity bar, per output tensor (atol, rtol): every element must satisfy
+# |x - ref| <= atol + rtol * |ref| (max-abs 2e-2 with relative 1e-2 for bf16;
+# 1e-5 / 1e-5 for fp32), and ||x - ref||_F / ||ref||_F <= rtol.  A pure
+# max-abs bound cannot hold for bf16 outputs of magnitude >= 8, whose
+# rounding alone (half a bf16 ulp, 2^-5 there) exceeds 2e-2.
 TOL = {"bf16": (2e-2, 1e-2), "fp32": (1e-5, 1e-5)}
 
 
@@ -43,11 +46,13 @@ def compare(name, got, ref, dtype="bf16"):
     # -inf entries (empty rows) must match exactly
     assert np.array_equal(got[~fin], ref[~fin]), f"{name}: non-finite values differ"
     diff = np.abs(got[fin] - ref[fin])
+    a_tol, r_tol = TOL[dtype]
     max_abs = float(diff.max(initial=0.0))
+    bound = a_tol + r_tol * np.abs(ref[fin])
+    worst = float((diff / bound).max(initial=0.0))
     denom = float(np.sqrt((ref[fin] ** 2).sum()))
     rel = float(np.sqrt((diff ** 2).sum()) / denom) if denom > 0 else max_abs
-    a_tol, r_tol = TOL[dtype]
-    log(f"  {name}: max_abs={max_abs:.3e} rel_fro={rel:.3e}")
-    assert max_abs <= a_tol, f"{name}: max abs error {max_abs:.3e} > {a_tol}"
+    log(f"  {name}: max_abs={max_abs:.3e} worst(|d|/(atol+rtol|ref|))={worst:.3f} rel_fro={rel:.3e}")
+    assert worst <= 1.0, f"{name}: |x - ref| exceeds {a_tol} + {r_tol}|ref| (worst ratio {worst:.3f})"
     assert rel <= r_tol, f"{name}: relative Frobenius error {rel:.3e} > {r_tol}"
     return max_abs, rel

@@ -182,3 +182,27 @@ def test_decode_argument_errors_on_host():
     assert lib.cowa_decode_workspace_size(ctypes.byref(bad), ctypes.byref(n)) == abi.COWA_ERR_INVALID_ARG
     bad = cowa.make_decode_params(4, 8, 2, 128, 1000, 16, 64, split_keys=100)
     assert lib.cowa_decode_workspace_size(ctypes.byref(bad), ctypes.byref(n)) == abi.COWA_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("case", [(1, 512, 512, 4, 2, 16, 64, 2, 0), (1, 8192, 8192, 32, 8, 64, 1024, 8, 0),
+                                  (2, 300, 1000, 6, 3, 5, 77, 8, 4), (1, 50, 50, 2, 2, 0, 0, 2, 0)])
+def test_legal_pairs_match_oracle(case):
+    from oracle import counts
+    bsz, n_q, n_k, h_q, h_k, ws, wn, ht, ho = case
+    p = cowa.make_params(bsz, n_q, n_k, h_q, h_k, 128, ws, wn, 64, 64, h_k_total=ht, h_k_offset=ho)
+    assert abi.cowa_legal_pairs(p) == counts.legal_pairs(bsz, n_q, n_k, h_q, h_k, ws, wn, ht, ho)
+
+
+def test_legal_pairs_128k_workload():
+    p = cowa.make_params(1, 131072, 131072, 32, 8, 128, 128, 4096, 128, 128)
+    assert abi.cowa_legal_pairs(p) == 49612416768
+
+
+def test_decode_visible_keys_match_oracle():
+    from oracle import counts
+    d = cowa.make_decode_params(5, 8, 2, 128, 5000, 16, 300, h_k_total=4, h_k_offset=1)
+    lens = [5000, 1, 316, 4000, 0]
+    ref = counts.decode_visible_keys([x for x in lens if 1 <= x <= 5000], 16, 300, 2, 4, 1).sum()
+    assert abi.cowa_decode_visible_keys(d, lens) == ref
+    d = cowa.make_decode_params(64, 32, 8, 128, 131072, 128, 4096)
+    assert abi.cowa_decode_visible_keys(d, [131072] * 64) == 64 * 8 * 20080
