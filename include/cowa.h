@@ -70,7 +70,7 @@ typedef struct {
   int32_t h_k_total;      /* global KV heads (>= h_k_offset + h_k) */
   int32_t h_k_offset;     /* global index of local KV head 0 */
   int32_t tile_q, tile_k; /* block sizes B_q, B_k: 32, 64 or 128 */
-  float softmax_scale;    /* multiplies Q K^T (1/sqrt(d) for the standard scale) */
+  float softmax_scale;    /* > 0, multiplies Q K^T (1/sqrt(d) for the standard scale) */
   int32_t dtype;          /* cowa_dtype */
 } cowa_params;
 
@@ -105,8 +105,8 @@ typedef struct {
   int32_t w_sink, w_near; /* >= 0 */
   int32_t h_k_total, h_k_offset;
   int32_t split_keys;     /* visible keys per split program; 0 = library default */
-  float softmax_scale;
-  int32_t dtype;          /* COWA_BF16 or COWA_FP32 */
+  float softmax_scale;    /* > 0 */
+  int32_t dtype;          /* COWA_BF16 */
 } cowa_decode_params;
 
 /* Library version string. */

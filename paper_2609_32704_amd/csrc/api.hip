@@ -44,7 +44,8 @@ cowa_status check_params(const cowa_params* p) {
   if (p->head_dim != 64 && p->head_dim != 128)
     return fail(COWA_ERR_UNSUPPORTED, "head_dim must be 64 or 128 (got %d)", p->head_dim);
   if (p->dtype != COWA_BF16 && p->dtype != COWA_FP32) return fail(COWA_ERR_INVALID_ARG, "unknown dtype %d", p->dtype);
-  if (!std::isfinite(p->softmax_scale)) return fail(COWA_ERR_INVALID_ARG, "softmax_scale must be finite");
+  if (!std::isfinite(p->softmax_scale) || !(p->softmax_scale > 0.f))
+    return fail(COWA_ERR_INVALID_ARG, "softmax_scale must be finite and > 0");
   return COWA_OK;
 }
 
@@ -344,7 +345,8 @@ static cowa_status check_decode_params(const cowa_decode_params* p) {
   if (p->dtype != COWA_BF16) return fail(COWA_ERR_UNSUPPORTED, "decode is built for bf16 only");
   if (!cowa::decode_supported(p->head_dim, p->h_q / p->h_k))
     return fail(COWA_ERR_UNSUPPORTED, "decode is built for QO-head groups of 1, 2, 4 or 8");
-  if (!std::isfinite(p->softmax_scale)) return fail(COWA_ERR_INVALID_ARG, "softmax_scale must be finite");
+  if (!std::isfinite(p->softmax_scale) || !(p->softmax_scale > 0.f))
+    return fail(COWA_ERR_INVALID_ARG, "softmax_scale must be finite and > 0");
   return COWA_OK;
 }
 

@@ -1,21 +1,27 @@
 // CoWA forward in bfloat16 on the CDNA4 matrix cores (Alg. 1).
 //
-// One workgroup of four 64-lane waves per (QO block i, QO head h, sequence b);
-// wave w owns queries [w * BQ/4, (w+1) * BQ/4) of the block.  For every KV
-// block j of J_{h_k}(i), visited in the schedule's descending order:
+// Work decomposition.  One workgroup per (QO block i, group of HPW QO heads
+// that share one KV head, sequence b): every QO head of a GQA group has the
+// same block set J_{h_k}(i), so the heads of a workgroup share each K/V block
+// staged in LDS.  Each 64-lane wave owns NQW query rows of one head (up to
+// 256 rows and 8 waves per workgroup).
 //
-//   * K_j is staged in LDS row-major ([key][d], 16-byte padded rows) and V_j
-//     transposed ([d][key]), both with coalesced 16-byte global loads;
-//   * S^T = K_j Q^T on v_mfma_f32_16x16x32_bf16 (fp32 accumulate), with Q^T
-//     held in registers for the whole block;
+// Per KV block j of J_{h_k}(i), visited in the schedule's descending order:
+//   * K_j and V_j are copied global -> LDS with direct 16-byte loads
+//     (global_load_lds), double buffered: block e+1 is in flight while block e
+//     is computed.  Rows are stored unpadded with their 16-byte chunks XOR
+//     swizzled by row, so both the row reads of K and the transposed reads of
+//     V hit distinct banks.
+//   * S^T = K_j Q^T on v_mfma_f32_16x16x32_bf16 (fp32 accumulate); Q^T stays
+//     in registers for the whole block.  Computing the transpose puts one
+//     query per lane column, which is the B-operand layout of the second
+//     product, so P never leaves registers.
 //   * only blocks flagged partial evaluate the element mask of Eq. fwa_support;
-//   * online softmax per query column in registers (running max m, running
-//     sum l, rescale of the O accumulator), base-2 with scale * log2(e) folded
-//     into the scores;
-//   * O^T += V_j^T P^T on the matrix cores, P rounded to bf16.  S^T is
-//     computed transposed so that its accumulator layout (query = lane % 16)
-//     is already the B-operand layout of the second product.
-//
+//   * online softmax in registers, base 2, with scale * log2(e) folded into one
+//     fused multiply-add per score; the O accumulator is rescaled only when a
+//     running maximum moved;
+//   * O^T += V_j^T P^T; the V^T fragments come straight from the row-major
+//     V_j in LDS through the transposing LDS read (ds_read_b64_tr_b16).
 // Finally O = O / l and LSE = (m + log2 l) ln 2 (natural log).
 #include "internal.h"
 #include "window_rule.h"
@@ -25,7 +31,10 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -41,194 +50,227 @@ __device__ inline int xcd_remap(int id, int total) {
   return chunk * 8 + (slot & 7);
 }
 
-template <int D, int BQ, int BK>
-struct FwdCfg {
-  static constexpr int NW = 4;
-  static constexpr int NQW = BQ / NW;   // queries per wave
-  static constexpr int NTQ = NQW / 16;  // 16-wide query tiles per wave
-  static constexpr int MTK = BK / 16;   // key tiles of S^T
-  static constexpr int KSD = D / 32;    // k-steps over d
-  static constexpr int MTD = D / 16;    // d tiles of O^T
-  static constexpr int KSK = BK / 32;   // k-steps over keys
-  static constexpr int KPAD = D + 8;    // Ks row stride (elements)
-  static constexpr int VPAD = BK + 4;   // Vt row stride (elements)
-  static constexpr int LDS_BYTES = (BK * KPAD + D * VPAD) * 2;
+template <int D, int BK>
+struct Tile {
+  static constexpr int CH = D / 8;                 // 16-byte chunks per row
+  static constexpr int BYTES = BK * D * 2;         // one K or V block
+  static constexpr int LOADS = BYTES / 1024;       // 1 KB direct loads per block
+  // byte offset of (row, 16-byte chunk) inside a swizzled block
+  __device__ static inline int off(int row, int chunk) { return row * (D * 2) + ((chunk ^ (row % CH)) << 4); }
 };
 
-template <int D, int BQ, int BK>
-__global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView sv, const __bf16* __restrict__ q,
-                                                       const __bf16* __restrict__ k, const __bf16* __restrict__ v,
-                                                       __bf16* __restrict__ o, float* __restrict__ lse) {
-  using C = FwdCfg<D, BQ, BK>;
-  extern __shared__ __align__(16) unsigned char smem[];
-  __bf16* Ks = reinterpret_cast<__bf16*>(smem);
-  __bf16* Vt = Ks + BK * C::KPAD;
+// Copy rows [k_first, k_first + BK) of a [n_k][D] bf16 matrix into a swizzled
+// LDS block; rows past n_k repeat the last row (they are masked later).
+template <int D, int BK>
+__device__ inline void load_block(const __bf16* base, int64_t k_first, int n_k, unsigned char* lds_block, int wave,
+                                  int nw, int lane) {
+  using T = Tile<D, BK>;
+  for (int n = wave; n < T::LOADS; n += nw) {
+    const int flat = n * 64 + lane;           // 16-byte unit index = LDS position
+    const int row = flat / T::CH, slot = flat % T::CH;
+    const int chunk = slot ^ (row % T::CH);   // global chunk stored at that position
+    int64_t kp = k_first + row;
+    if (kp >= n_k) kp = n_k - 1;
+    const __bf16* src = base + kp * D + chunk * 8;
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src),
+                                     (lds_void*)(lds_block + n * 1024), 16, 0, 0);
+  }
+}
 
-  const int total = sv.n_qt * p.h_q * p.batch;
+template <int D, int BQ, int BK, int NQW>
+__global__ void __launch_bounds__(512) fwd_bf16_kernel(cowa_params p, SchedView sv, int hpw, int n_hgroups,
+                                                       const __bf16* __restrict__ q, const __bf16* __restrict__ k,
+                                                       const __bf16* __restrict__ v, __bf16* __restrict__ o,
+                                                       float* __restrict__ lse) {
+  using T = Tile<D, BK>;
+  constexpr int NTQ = NQW / 16;           // query tiles per wave
+  constexpr int BKC = BK > 64 ? 64 : BK;   // keys per softmax step (a KV block is 1 or 2 steps)
+  constexpr int MTK = BKC / 16;           // key tiles of S^T
+  constexpr int KSD = D / 32;             // k-steps over d
+  constexpr int MTD = D / 16;             // d tiles of O^T
+  constexpr int KSK = BKC / 32;           // k-steps over keys
+  constexpr int WAVES_PER_HEAD = BQ / NQW;
+  extern __shared__ __align__(1024) unsigned char smem[];
+
+  const int nw = blockDim.x >> 6;
+  const int G = p.h_q / p.h_k;
+  const int total = sv.n_qt * n_hgroups * p.batch;
   const int work = xcd_remap(blockIdx.x, total);
-  const int hb = p.h_q * p.batch;
-  const int i = sv.n_qt - 1 - work / hb;  // latest (longest) QO blocks first
-  const int h = (work % hb) % p.h_q, b = (work % hb) / p.h_q;
-  const int hk = (int)(((int64_t)h * p.h_k) / p.h_q);
-  const HeadGeo g = make_geo(p.n_q, p.n_k, p.w_sink, p.w_near, BQ, BK, p.h_k_offset + hk, p.h_k_total);
+  const int per_i = n_hgroups * p.batch;
+  const int i = sv.n_qt - 1 - work / per_i;  // latest (longest) QO blocks first
+  const int rest = work % per_i;
+  const int hgi = rest % n_hgroups, b = rest / n_hgroups;
+  const int hk = hgi / (G / hpw);
+  const int h0 = hgi * hpw;  // first QO head of this workgroup (all in KV group hk)
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int lr = lane & 15, lg = lane >> 4;
-  const int64_t q_first = (int64_t)i * BQ + wave * C::NQW;
+  const int h = h0 + wave / WAVES_PER_HEAD;
+  const int64_t q_first = (int64_t)i * BQ + (wave % WAVES_PER_HEAD) * NQW;
+  const Geo32 g = geo32(make_geo(p.n_q, p.n_k, p.w_sink, p.w_near, BQ, BK, p.h_k_offset + hk, p.h_k_total));
 
   const __bf16* kbase = k + ((int64_t)b * p.h_k + hk) * p.n_k * D;
   const __bf16* vbase = v + ((int64_t)b * p.h_k + hk) * p.n_k * D;
-
-  // Q^T fragments (B operand): query column nt*16 + lr, d = ks*32 + 8*lg + 0..7.
-  bf16x8 qf[C::NTQ][C::KSD];
-#pragma unroll
-  for (int nt = 0; nt < C::NTQ; ++nt) {
-    const int64_t qp = q_first + nt * 16 + lr;
-    const __bf16* qrow = q + (((int64_t)b * p.h_q + h) * p.n_q + (qp < p.n_q ? qp : 0)) * D;
-#pragma unroll
-    for (int ks = 0; ks < C::KSD; ++ks) {
-      bf16x8 val = *reinterpret_cast<const bf16x8*>(qrow + ks * 32 + 8 * lg);
-      if (qp >= p.n_q) val = bf16x8{};
-      qf[nt][ks] = val;
-    }
-  }
-
-  f32x4 oacc[C::MTD][C::NTQ];
-#pragma unroll
-  for (int md = 0; md < C::MTD; ++md)
-#pragma unroll
-    for (int nt = 0; nt < C::NTQ; ++nt) oacc[md][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run[C::NTQ], l_run[C::NTQ];
-#pragma unroll
-  for (int nt = 0; nt < C::NTQ; ++nt) { m_run[nt] = -INFINITY; l_run[nt] = 0.f; }
-
-  const float c = p.softmax_scale * kLog2e;
   const int r = hk * sv.n_qt + i;
   const int e0 = sv.fwd_row_ptr[r], e1 = sv.fwd_row_ptr[r + 1];
 
+  // buffer s: K at smem + 2 s BYTES, V right after it
+  if (e0 < e1) {
+    const int64_t kf = (int64_t)(sv.fwd_ent[e0] >> 1) * BK;
+    load_block<D, BK>(kbase, kf, p.n_k, smem, wave, nw, lane);
+    load_block<D, BK>(vbase, kf, p.n_k, smem + T::BYTES, wave, nw, lane);
+  }
+
+  // Q^T fragments (B operand): query column nt*16 + lr, d = ks*32 + 8*lg + 0..7
+  bf16x8 qf[NTQ][KSD];
+#pragma unroll
+  for (int nt = 0; nt < NTQ; ++nt) {
+    const int64_t qp = q_first + nt * 16 + lr;
+    const bool ok = qp < p.n_q;
+    const __bf16* qrow = q + (((int64_t)b * p.h_q + h) * p.n_q + (ok ? qp : 0)) * D;
+#pragma unroll
+    for (int ks = 0; ks < KSD; ++ks) {
+      bf16x8 val = *reinterpret_cast<const bf16x8*>(qrow + ks * 32 + 8 * lg);
+      qf[nt][ks] = ok ? val : bf16x8{};
+    }
+  }
+
+  f32x4 oacc[MTD][NTQ];
+#pragma unroll
+  for (int md = 0; md < MTD; ++md)
+#pragma unroll
+    for (int nt = 0; nt < NTQ; ++nt) oacc[md][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run[NTQ], l_run[NTQ];
+#pragma unroll
+  for (int nt = 0; nt < NTQ; ++nt) { m_run[nt] = -INFINITY; l_run[nt] = 0.f; }
+  const float c = p.softmax_scale * kLog2e;
+
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+
   for (int e = e0; e < e1; ++e) {
+    const int buf = (e - e0) & 1;
     const uint32_t ent = sv.fwd_ent[e];
     const int j = (int)(ent >> 1);
     const bool partial = ent & 1u;
     const int64_t k_first = (int64_t)j * BK;
-
-    __syncthreads();  // previous block's LDS reads are done
-    // K_j -> Ks[key][d]
-    for (int x = tid; x < BK * (D / 8); x += 256) {
-      const int key = x / (D / 8), ch = x % (D / 8);
-      const int64_t kp = k_first + key;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (kp < p.n_k) val = *reinterpret_cast<const uint4*>(kbase + kp * D + ch * 8);
-      *reinterpret_cast<uint4*>(Ks + key * C::KPAD + ch * 8) = val;
+    if (e + 1 < e1) {  // prefetch the next block into the other buffer
+      const int64_t kf = (int64_t)(sv.fwd_ent[e + 1] >> 1) * BK;
+      unsigned char* nb = smem + (buf ^ 1) * 2 * T::BYTES;
+      load_block<D, BK>(kbase, kf, p.n_k, nb, wave, nw, lane);
+      load_block<D, BK>(vbase, kf, p.n_k, nb + T::BYTES, wave, nw, lane);
     }
-    // V_j -> Vt[d][key], four keys x eight d per unit
-    for (int x = tid; x < (BK / 4) * (D / 8); x += 256) {
-      const int kg = x / (D / 8), ch = x % (D / 8);
-      uint4 rv[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int64_t kp = k_first + kg * 4 + u;
-        rv[u] = make_uint4(0, 0, 0, 0);
-        if (kp < p.n_k) rv[u] = *reinterpret_cast<const uint4*>(vbase + kp * D + ch * 8);
-      }
-      const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&rv[0]);
-      const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&rv[1]);
-      const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&rv[2]);
-      const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&rv[3]);
-#pragma unroll
-      for (int dd = 0; dd < 8; ++dd) {
-        const int wd = dd >> 1;
-        uint2 pk;
-        if (dd & 1) {
-          pk.x = (w0[wd] >> 16) | (w1[wd] & 0xffff0000u);
-          pk.y = (w2[wd] >> 16) | (w3[wd] & 0xffff0000u);
-        } else {
-          pk.x = (w0[wd] & 0xffffu) | (w1[wd] << 16);
-          pk.y = (w2[wd] & 0xffffu) | (w3[wd] << 16);
-        }
-        *reinterpret_cast<uint2*>(Vt + (ch * 8 + dd) * C::VPAD + kg * 4) = pk;
-      }
-    }
-    __syncthreads();
+    const unsigned char* Kt = smem + buf * 2 * T::BYTES;
+    const unsigned char* Vt = Kt + T::BYTES;
 
-    // S^T = K_j Q^T : rows = keys (mt*16 + 4*lg + rr), column = query nt*16 + lr
-    f32x4 sacc[C::MTK][C::NTQ];
-#pragma unroll
-    for (int mt = 0; mt < C::MTK; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < C::NTQ; ++nt) sacc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < C::KSD; ++ks)
-#pragma unroll
-      for (int mt = 0; mt < C::MTK; ++mt) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(Ks + (mt * 16 + lr) * C::KPAD + ks * 32 + 8 * lg);
-#pragma unroll
-        for (int nt = 0; nt < C::NTQ; ++nt)
-          sacc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[nt][ks], sacc[mt][nt], 0, 0, 0);
-      }
-
-    // online softmax per query column
-#pragma unroll
-    for (int nt = 0; nt < C::NTQ; ++nt) {
-      const int64_t qp = q_first + nt * 16 + lr;
-      float mx = -INFINITY;
-#pragma unroll
-      for (int mt = 0; mt < C::MTK; ++mt)
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          float s = sacc[mt][nt][rr] * c;
-          if (partial && !legal_pair(g, qp, k_first + mt * 16 + 4 * lg + rr)) s = -INFINITY;
-          sacc[mt][nt][rr] = s;
-          mx = fmaxf(mx, s);
+#pragma unroll 1
+    for (int kc = 0; kc < BK; kc += BKC) {
+      // S^T = K_j Q^T : rows = keys (mt*16 + 4*lg + rr), column = query nt*16 + lr
+      f32x4 sacc[MTK][NTQ];
+  #pragma unroll
+      for (int mt = 0; mt < MTK; ++mt)
+  #pragma unroll
+        for (int nt = 0; nt < NTQ; ++nt) sacc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  #pragma unroll
+      for (int ks = 0; ks < KSD; ++ks)
+  #pragma unroll
+        for (int mt = 0; mt < MTK; ++mt) {
+          const int row = kc + mt * 16 + lr;
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(Kt + T::off(row, ks * 4 + lg));
+  #pragma unroll
+          for (int nt = 0; nt < NTQ; ++nt)
+            sacc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[nt][ks], sacc[mt][nt], 0, 0, 0);
         }
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run[nt], mx);
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = __builtin_amdgcn_exp2f(m_run[nt] - m_use);
-      m_run[nt] = m_new;
-      float lsum = 0.f;
-#pragma unroll
-      for (int mt = 0; mt < C::MTK; ++mt)
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          const float pv = __builtin_amdgcn_exp2f(sacc[mt][nt][rr] - m_use);
-          sacc[mt][nt][rr] = pv;
-          lsum += pv;
-        }
-      l_run[nt] = l_run[nt] * alpha + lsum;
-#pragma unroll
-      for (int md = 0; md < C::MTD; ++md) oacc[md][nt] *= alpha;
-    }
 
-    // O^T += V_j^T P^T : k-slot s of step ks is key 32ks + 4lg + s (s < 4) or 32ks + 16 + 4lg + (s - 4)
-#pragma unroll
-    for (int ks = 0; ks < C::KSK; ++ks) {
-      bf16x8 pb[C::NTQ];
-#pragma unroll
-      for (int nt = 0; nt < C::NTQ; ++nt) {
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          pb[nt][rr] = (__bf16)sacc[2 * ks][nt][rr];
-          pb[nt][4 + rr] = (__bf16)sacc[2 * ks + 1][nt][rr];
+      // online softmax per query column (raw-score units; c folded into the exponent)
+      if (partial) {
+  #pragma unroll
+        for (int nt = 0; nt < NTQ; ++nt) {
+          const int qp = (int)q_first + nt * 16 + lr;
+          const int k0 = (int)k_first + kc + 4 * lg;
+  #pragma unroll
+          for (int mt = 0; mt < MTK; ++mt)
+  #pragma unroll
+            for (int rr = 0; rr < 4; ++rr)
+              // an add that reads the accumulator: a plain masked store of -inf
+              // into an MFMA destination could be overtaken by the MFMA write
+              sacc[mt][nt][rr] += legal32(g, qp, k0 + mt * 16 + rr) ? 0.f : -INFINITY;
         }
       }
-#pragma unroll
-      for (int md = 0; md < C::MTD; ++md) {
-        const __bf16* vr = Vt + (md * 16 + lr) * C::VPAD + ks * 32 + 4 * lg;
-        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vr);
-        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vr + 16);
-        const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-#pragma unroll
-        for (int nt = 0; nt < C::NTQ; ++nt)
-          oacc[md][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[nt], oacc[md][nt], 0, 0, 0);
+      float alpha[NTQ];
+      bool moved = false;
+  #pragma unroll
+      for (int nt = 0; nt < NTQ; ++nt) {
+        float mx = -INFINITY;
+  #pragma unroll
+        for (int mt = 0; mt < MTK; ++mt)
+  #pragma unroll
+          for (int rr = 0; rr < 4; ++rr) mx = fmaxf(mx, sacc[mt][nt][rr]);
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float m_new = fmaxf(m_run[nt], mx);
+        moved |= m_new > m_run[nt];
+        const float mc = m_new == -INFINITY ? 0.f : m_new * c;
+        alpha[nt] = __builtin_amdgcn_exp2f(m_run[nt] * c - mc);
+        m_run[nt] = m_new;
+        float lsum = 0.f;
+  #pragma unroll
+        for (int mt = 0; mt < MTK; ++mt)
+  #pragma unroll
+          for (int rr = 0; rr < 4; ++rr) {
+            const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[mt][nt][rr], c, -mc));
+            sacc[mt][nt][rr] = pv;
+            lsum += pv;
+          }
+        l_run[nt] = l_run[nt] * alpha[nt] + lsum;
+      }
+      if (__any(moved)) {
+  #pragma unroll
+        for (int md = 0; md < MTD; ++md)
+  #pragma unroll
+          for (int nt = 0; nt < NTQ; ++nt) oacc[md][nt] *= alpha[nt];
+      }
+
+      // O^T += V_j^T P^T.  k-slot t of step ks is key 32ks + 4lg + t (t < 4) or
+      // 32ks + 16 + 4lg + (t - 4); the transposing read gives lane lr the column
+      // d = md*16 + lr of four keys, supplied by lanes 4*t + (lr / 4) of its group.
+      const int sup_key = 4 * lg + (lr >> 2);
+      const int sup_dq = lr & 3;
+  #pragma unroll
+      for (int ks = 0; ks < KSK; ++ks) {
+        bf16x8 pb[NTQ];
+  #pragma unroll
+        for (int nt = 0; nt < NTQ; ++nt)
+  #pragma unroll
+          for (int rr = 0; rr < 4; ++rr) {
+            pb[nt][rr] = (__bf16)sacc[2 * ks][nt][rr];
+            pb[nt][4 + rr] = (__bf16)sacc[2 * ks + 1][nt][rr];
+          }
+        const int row0 = kc + ks * 32 + sup_key, row1 = row0 + 16;
+  #pragma unroll
+        for (int md = 0; md < MTD; ++md) {
+          const int byte = (md * 16 + 4 * sup_dq) * 2;  // within the row
+          const int chunk = byte >> 4, half = byte & 15;
+          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_i16x4*)(Vt + T::off(row0, chunk) + half));
+          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_i16x4*)(Vt + T::off(row1, chunk) + half));
+          const bf16x4 lob = __builtin_bit_cast(bf16x4, lo), hib = __builtin_bit_cast(bf16x4, hi);
+          const bf16x8 a = {lob[0], lob[1], lob[2], lob[3], hib[0], hib[1], hib[2], hib[3]};
+  #pragma unroll
+          for (int nt = 0; nt < NTQ; ++nt)
+            oacc[md][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[nt], oacc[md][nt], 0, 0, 0);
+        }
       }
     }
+
+    __builtin_amdgcn_s_waitcnt(0);  // the prefetch of block e+1 has landed
+    __syncthreads();                 // ... for every wave, and block e is no longer read
   }
 
-  // O = O / l; LSE = (m + log2 l) ln 2
+  // O = O / l; LSE = (m c + log2 l) ln 2
 #pragma unroll
-  for (int nt = 0; nt < C::NTQ; ++nt) {
+  for (int nt = 0; nt < NTQ; ++nt) {
     float lt = l_run[nt];
     lt += __shfl_xor(lt, 16);
     lt += __shfl_xor(lt, 32);
@@ -237,31 +279,37 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
     __bf16* orow = o + (((int64_t)b * p.h_q + h) * p.n_q + qp) * D;
 #pragma unroll
-    for (int md = 0; md < C::MTD; ++md) {
+    for (int md = 0; md < MTD; ++md) {
       bf16x4 ov;
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) ov[rr] = (__bf16)(oacc[md][nt][rr] * inv);
       *reinterpret_cast<bf16x4*>(orow + md * 16 + 4 * lg) = ov;
     }
     if (lg == 0)
-      lse[((int64_t)b * p.h_q + h) * p.n_q + qp] = lt > 0.f ? (m_run[nt] + __log2f(lt)) * kLn2 : -INFINITY;
+      lse[((int64_t)b * p.h_q + h) * p.n_q + qp] = lt > 0.f ? (m_run[nt] * c + __log2f(lt)) * kLn2 : -INFINITY;
   }
 }
 
-template <int D, int BQ, int BK>
+template <int D, int BQ, int BK, int NQW = 32>
 hipError_t launch_cfg(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
                       void* o, float* lse, hipStream_t stream) {
-  using C = FwdCfg<D, BQ, BK>;
-  auto kern = fwd_bf16_kernel<D, BQ, BK>;
+  constexpr int LDS = 4 * Tile<D, BK>::BYTES;
+  static_assert(LDS <= 160 * 1024, "LDS budget");
+  auto kern = fwd_bf16_kernel<D, BQ, BK, NQW>;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
     if (err != hipSuccess) return err;
     attr_set = true;
   }
-  const unsigned blocks = (unsigned)sv.n_qt * p.h_q * p.batch;
-  hipLaunchKernelGGL(kern, dim3(blocks), dim3(256), C::LDS_BYTES, stream, p, sv,
+  const int G = p.h_q / p.h_k;
+  int hpw = 256 / BQ;  // QO heads per workgroup: up to 256 query rows
+  while (hpw > 1 && G % hpw != 0) hpw >>= 1;
+  const int n_hgroups = p.h_q / hpw;
+  const int waves = hpw * (BQ / NQW);
+  const unsigned blocks = (unsigned)sv.n_qt * n_hgroups * p.batch;
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * waves), LDS, stream, p, sv, hpw, n_hgroups,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), static_cast<const __bf16*>(v),
                      static_cast<__bf16*>(o), lse);
   return hipGetLastError();

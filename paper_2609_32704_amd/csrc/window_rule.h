@@ -53,6 +53,30 @@ __host__ __device__ inline bool legal_pair(const HeadGeo& g, int64_t q, int64_t 
   return d < g.w_near || k < g.w_sink || (d >= g.lo && d < g.hi);
 }
 
+// 32-bit form of the element predicate for kernels: window bounds clamped to
+// n_k (a distance never reaches n_k, so a larger bound behaves the same).
+struct Geo32 {
+  int32_t off, w_near, w_sink, lo, hi, n_q, n_k;
+};
+
+__host__ __device__ inline Geo32 geo32(const HeadGeo& g) {
+  Geo32 r;
+  r.off = g.n_k - g.n_q;
+  r.w_near = g.w_near < g.n_k ? g.w_near : g.n_k;
+  r.w_sink = g.w_sink < g.n_k ? g.w_sink : g.n_k;
+  r.lo = (int32_t)imin64(g.lo, g.n_k);
+  r.hi = (int32_t)imin64(g.hi, g.n_k);
+  r.n_q = g.n_q;
+  r.n_k = g.n_k;
+  return r;
+}
+
+// Same predicate as legal_pair for in-range positions (q < n_q, k < n_k).
+__host__ __device__ inline bool legal32(const Geo32& g, int32_t q, int32_t k) {
+  const int32_t d = q + g.off - k;
+  return q < g.n_q && k < g.n_k && d >= 0 && (d < g.w_near || k < g.w_sink || (d >= g.lo && d < g.hi));
+}
+
 // Up to three inclusive ranges, merged (overlapping or adjacent ranges join).
 struct Ranges {
   int32_t n;

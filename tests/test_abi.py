@@ -92,7 +92,8 @@ def _status(fn, *args):
     ("w_near", -5, abi.COWA_ERR_INVALID_ARG), ("h_k_offset", 1, abi.COWA_ERR_INVALID_ARG),
     ("h_k_total", 1, abi.COWA_ERR_INVALID_ARG), ("head_dim", 96, abi.COWA_ERR_UNSUPPORTED),
     ("dtype", 7, abi.COWA_ERR_INVALID_ARG), ("batch", -1, abi.COWA_ERR_INVALID_ARG),
-    ("softmax_scale", float("inf"), abi.COWA_ERR_INVALID_ARG),
+    ("softmax_scale", float("inf"), abi.COWA_ERR_INVALID_ARG), ("softmax_scale", 0.0, abi.COWA_ERR_INVALID_ARG),
+    ("softmax_scale", -0.125, abi.COWA_ERR_INVALID_ARG),
 ])
 def test_invalid_params_rejected_on_host(field, value, status):
     lib = _lib()
