@@ -3,8 +3,8 @@
 
 One step is one pass of the whole hot path over one batch of synthetic input:
 
-  window tuples (host) -> schedule build -> forward -> backward (prepare, main,
-  finish) at 131072 tokens, bf16, B=1, H_q=32, H_k=8, d=128, sink 128, near
+  window tuples (host) -> schedule build -> forward -> backward (prepare, dK/dV
+  pass, dQ pass) at 131072 tokens, bf16, B=1, H_q=32, H_k=8, d=128, sink 128, near
   4096, 128x128 blocks; then one decoding step over 64 sequences x 131072
   cached tokens with the same heads and windows.
 
@@ -181,7 +181,7 @@ def main():
     vis_keys = _abi.cowa_decode_visible_keys(dpar, seqlens_host)
     dec_bytes = 2 * vis_keys * D["d"] * 2 + D["batch"] * D["h_q"] * (2 * D["d"] * 2 + 4)
 
-    names = ["schedule", "fwd", "bwd_prepare", "bwd_main", "bwd_finish", "decode"]
+    names = ["schedule", "fwd", "bwd_prepare", "bwd_main", "bwd_dq", "decode"]
 
     def step(evs):
         evs[0].record()
@@ -195,7 +195,8 @@ def main():
         _abi.cowa_bwd_main(p, sched.s, q.data_ptr(), k.data_ptr(), v.data_ptr(), lse.data_ptr(), do.data_ptr(),
                            dk.data_ptr(), dv.data_ptr(), ws.data_ptr(), ws_bytes, stream)
         evs[4].record()
-        _abi.cowa_bwd_finish(p, dq.data_ptr(), ws.data_ptr(), ws_bytes, stream)
+        _abi.cowa_bwd_dq(p, sched.s, q.data_ptr(), k.data_ptr(), v.data_ptr(), lse.data_ptr(), do.data_ptr(),
+                         dq.data_ptr(), ws.data_ptr(), ws_bytes, stream)
         evs[5].record()
         _abi.cowa_decode(dpar, dq_in.data_ptr(), kc.data_ptr(), vc.data_ptr(), seqlens.data_ptr(), od.data_ptr(),
                          lsed.data_ptr(), dws.data_ptr(), dws.numel(), stream)
@@ -221,7 +222,7 @@ def main():
         for idx, n in enumerate(names):
             per[n] += evs[idx].elapsed_time(evs[idx + 1])
     per = {n: per[n] / args.steps for n in names}
-    bwd_ms = per["bwd_prepare"] + per["bwd_main"] + per["bwd_finish"]
+    bwd_ms = per["bwd_prepare"] + per["bwd_main"] + per["bwd_dq"]
     train_ms = per["schedule"] + per["fwd"] + bwd_ms
     value = (fwd_flops + bwd_flops) / (train_ms * 1e-3) / 1e12
 
@@ -231,13 +232,16 @@ def main():
         "schedule": {"ms": per["schedule"], "bound": "launch", "note": "three small kernels"},
         "fwd": {"ms": per["fwd"], "bound": "mfma", "work": fwd_flops, "unit": "TFLOP/s",
                 "achieved": fwd_flops / (per["fwd"] * 1e-3) / 1e12},
-        "bwd_prepare": {"ms": per["bwd_prepare"], "bound": "hbm", "unit": "GB/s",
-                        "work": 2 * elem_q * 2 + rows_q * 4 + elem_q * 4,
-                        "achieved": (2 * elem_q * 2 + rows_q * 4 + elem_q * 4) / (per["bwd_prepare"] * 1e-3) / 1e9},
-        "bwd_main": {"ms": per["bwd_main"], "bound": "mfma", "work": bwd_flops, "unit": "TFLOP/s",
-                     "achieved": bwd_flops / (per["bwd_main"] * 1e-3) / 1e12},
-        "bwd_finish": {"ms": per["bwd_finish"], "bound": "hbm", "unit": "GB/s", "work": elem_q * 4 + elem_q * 2,
-                       "achieved": (elem_q * 6) / (per["bwd_finish"] * 1e-3) / 1e9},
+        "bwd_prepare": {"ms": per["bwd_prepare"], "bound": "hbm", "unit": "GB/s", "work": 2 * elem_q * 2 + rows_q * 4,
+                        "achieved": (2 * elem_q * 2 + rows_q * 4) / (per["bwd_prepare"] * 1e-3) / 1e9},
+        # algorithmic share of the backward's 10d per pair: the dK/dV pass does the
+        # recompute of S and dP plus dV and dK (8d); the dQ pass adds dQ (2d) and
+        # recomputes S and dP again (4d executed on top, not counted)
+        "bwd_main": {"ms": per["bwd_main"], "bound": "mfma", "work": 8 * T["d"] * pairs, "unit": "TFLOP/s",
+                     "achieved": 8 * T["d"] * pairs / (per["bwd_main"] * 1e-3) / 1e12},
+        "bwd_dq": {"ms": per["bwd_dq"], "bound": "mfma", "work": 2 * T["d"] * pairs, "unit": "TFLOP/s",
+                   "achieved": 2 * T["d"] * pairs / (per["bwd_dq"] * 1e-3) / 1e12,
+                   "executed_tflops": 6 * T["d"] * pairs / (per["bwd_dq"] * 1e-3) / 1e12},
         "decode": {"ms": per["decode"], "bound": "hbm", "unit": "GB/s", "work": dec_bytes,
                    "achieved": dec_bytes / (per["decode"] * 1e-3) / 1e9},
     }
@@ -249,10 +253,10 @@ def main():
 
     main_k = kernels["bwd_main"]
     traffic = read_traffic("bwd_main")
-    roofline = {"kernel": "bwd_main (backward main pass, 131072 tokens)", "bound": "mfma",
+    roofline = {"kernel": "bwd_main (backward dK/dV pass, 131072 tokens)", "bound": "mfma",
                 "achieved": main_k["achieved"], "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": main_k["frac"], "traffic": traffic,
-                "work_per_launch": f"{bwd_flops:.4e} FLOP = 10 d x {pairs} legal pairs"}
+                "work_per_launch": f"{8 * T['d'] * pairs:.4e} FLOP = 8 d x {pairs} legal pairs"}
 
     dense = None
     if not args.no_dense and args.dense_iters > 0:

@@ -146,39 +146,44 @@ cowa_status cowa_fwd(const cowa_params* p, const cowa_schedule_t* s,
                      const void* q, const void* k, const void* v,
                      void* o, float* lse, void* stream);
 
-/* Workspace bytes cowa_bwd needs: the float32 dQ accumulator and the row
- * sums D = rowsum(O * dO). */
+/* Workspace bytes cowa_bwd needs: the float32 row sums D = rowsum(O * dO)
+ * of Alg. 2, one per query row. */
 cowa_status cowa_bwd_workspace_size(const cowa_params* p, size_t* bytes);
 
 /* Backward (Alg. 2): exact gradients of <dO, O> w.r.t. the unscaled Q, K and
  * V, using the saved O and LSE of the forward.  dq like q; dk/dv like k/v
  * (keys that no query sees get zero).  bf16 only; tile_q and tile_k in
- * {64, 128}.  Equivalent to cowa_bwd_prepare, cowa_bwd_main and
- * cowa_bwd_finish in that order on the same workspace. */
+ * {64, 128}.  Equivalent to cowa_bwd_prepare, cowa_bwd_main and cowa_bwd_dq in
+ * that order on the same workspace.  Deterministic: no atomics. */
 cowa_status cowa_bwd(const cowa_params* p, const cowa_schedule_t* s,
                      const void* q, const void* k, const void* v,
                      const void* o, const float* lse, const void* d_o,
                      void* dq, void* dk, void* dv,
                      void* workspace, size_t ws_bytes, void* stream);
 
-/* Backward stage 1: the row sums D = rowsum(O * dO) of Alg. 2 (the term
- * subtracted from dP) into the workspace, and the workspace's float32 dQ
- * accumulator set to zero. */
+/* Backward stage 1: D = rowsum(O * dO) (the term subtracted from dP in
+ * Alg. 2) into the workspace. */
 cowa_status cowa_bwd_prepare(const cowa_params* p, const void* o, const void* d_o,
                              void* workspace, size_t ws_bytes, void* stream);
 
-/* Backward stage 2 (the loop of Alg. 2): for every local KV head and KV block,
- * over every QO head of its group and every QO block of I_h(j) in ascending
- * order, recompute P from LSE, form dS, accumulate dK and dV of the block
- * (written once, no atomics) and add dS K into the dQ accumulator (float32
- * atomics).  Needs the workspace filled by cowa_bwd_prepare. */
+/* Backward stage 2, dK and dV (the loop of Alg. 2 over QO blocks): for every
+ * local KV head and KV block, over every QO head of its group and every QO
+ * block of I_h(j) in ascending order, recompute P from LSE, form dS, and
+ * accumulate dK and dV of the block, written once without atomics.  Needs
+ * the workspace filled by cowa_bwd_prepare. */
 cowa_status cowa_bwd_main(const cowa_params* p, const cowa_schedule_t* s,
                           const void* q, const void* k, const void* v,
                           const float* lse, const void* d_o, void* dk, void* dv,
                           void* workspace, size_t ws_bytes, void* stream);
 
-/* Backward stage 3: dq = bfloat16(dQ accumulator). */
-cowa_status cowa_bwd_finish(const cowa_params* p, void* dq, void* workspace, size_t ws_bytes, void* stream);
+/* Backward stage 3, dQ: for every QO head and QO block, over the KV blocks of
+ * J_h(i), recompute P and dS and accumulate dQ = scale dS K, written once.
+ * (Alg. 2 adds these contributions with atomics inside stage 2; a separate
+ * pass avoids them.)  Needs the workspace filled by cowa_bwd_prepare. */
+cowa_status cowa_bwd_dq(const cowa_params* p, const cowa_schedule_t* s,
+                        const void* q, const void* k, const void* v,
+                        const float* lse, const void* d_o, void* dq,
+                        void* workspace, size_t ws_bytes, void* stream);
 
 /* Workspace bytes of one decoding step: split partial states (m, l, O). */
 cowa_status cowa_decode_workspace_size(const cowa_decode_params* p, size_t* bytes);

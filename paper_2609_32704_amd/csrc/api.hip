@@ -249,12 +249,12 @@ cowa_status cowa_bwd_workspace_size(const cowa_params* p, size_t* bytes) {
   COWA_TRY(check_params(p));
   if (!bytes) return fail(COWA_ERR_INVALID_ARG, "bytes is NULL");
   const size_t rows = (size_t)p->batch * p->h_q * p->n_q;
-  *bytes = align256(rows * p->head_dim * sizeof(float)) + align256(rows * sizeof(float));
+  *bytes = align256(rows * sizeof(float));
   return COWA_OK;
 }
 
-// Common checks of the backward stages; fills the workspace views.
-static cowa_status check_bwd(const cowa_params* p, size_t ws_bytes, void* workspace, float** dq_acc, float** dsum) {
+// Common checks of the backward stages; the workspace holds D = rowsum(O * dO).
+static cowa_status check_bwd(const cowa_params* p, size_t ws_bytes, void* workspace, float** dsum) {
   COWA_TRY(check_params(p));
   if (p->dtype != COWA_BF16) return fail(COWA_ERR_UNSUPPORTED, "backward is built for bf16 only");
   if (!cowa::bwd_bf16_supported(p->head_dim, p->tile_q, p->tile_k))
@@ -264,61 +264,70 @@ static cowa_status check_bwd(const cowa_params* p, size_t ws_bytes, void* worksp
   COWA_TRY(cowa_bwd_workspace_size(p, &need));
   if (p->batch > 0 && (!workspace || ws_bytes < need || !aligned(workspace, 256)))
     return fail(COWA_ERR_WORKSPACE, "backward needs a 256-byte aligned workspace of %zu bytes (got %zu)", need, ws_bytes);
-  const size_t rows = (size_t)p->batch * p->h_q * p->n_q;
-  *dq_acc = static_cast<float*>(workspace);
-  *dsum = reinterpret_cast<float*>(static_cast<char*>(workspace) + align256(rows * p->head_dim * sizeof(float)));
+  *dsum = static_cast<float*>(workspace);
   return COWA_OK;
+}
+
+static cowa_status check_qkv_lse_do(const void* q, const void* k, const void* v, const float* lse, const void* d_o) {
+  COWA_TRY(check_tensor(q, "q", 16));
+  COWA_TRY(check_tensor(k, "k", 16));
+  COWA_TRY(check_tensor(v, "v", 16));
+  COWA_TRY(check_tensor(lse, "lse", 4));
+  return check_tensor(d_o, "d_o", 16);
 }
 
 cowa_status cowa_bwd_prepare(const cowa_params* p, const void* o, const void* d_o, void* workspace, size_t ws_bytes,
                              void* stream) {
-  float *dq_acc, *dsum;
-  COWA_TRY(check_bwd(p, ws_bytes, workspace, &dq_acc, &dsum));
+  float* dsum;
+  COWA_TRY(check_bwd(p, ws_bytes, workspace, &dsum));
   if (p->batch == 0) return COWA_OK;
   COWA_TRY(check_tensor(o, "o", 16));
   COWA_TRY(check_tensor(d_o, "d_o", 16));
   COWA_TRY(check_device());
-  return hip_status(cowa::launch_bwd_prepare(*p, o, d_o, dq_acc, dsum, static_cast<hipStream_t>(stream)),
+  return hip_status(cowa::launch_bwd_prepare(*p, o, d_o, dsum, static_cast<hipStream_t>(stream)),
                     "backward prepare launch");
 }
 
 cowa_status cowa_bwd_main(const cowa_params* p, const cowa_schedule_t* s, const void* q, const void* k,
                           const void* v, const float* lse, const void* d_o, void* dk, void* dv, void* workspace,
                           size_t ws_bytes, void* stream) {
-  float *dq_acc, *dsum;
-  COWA_TRY(check_bwd(p, ws_bytes, workspace, &dq_acc, &dsum));
+  float* dsum;
+  COWA_TRY(check_bwd(p, ws_bytes, workspace, &dsum));
   COWA_TRY(check_schedule(p, s));
   if (p->batch == 0) return COWA_OK;
-  COWA_TRY(check_tensor(q, "q", 16));
-  COWA_TRY(check_tensor(k, "k", 16));
-  COWA_TRY(check_tensor(v, "v", 16));
-  COWA_TRY(check_tensor(lse, "lse", 4));
-  COWA_TRY(check_tensor(d_o, "d_o", 16));
+  COWA_TRY(check_qkv_lse_do(q, k, v, lse, d_o));
   COWA_TRY(check_tensor(dk, "dk", 16));
   COWA_TRY(check_tensor(dv, "dv", 16));
   if ((int64_t)s->n_kt * p->h_k * p->batch >= (int64_t(1) << 31))
     return fail(COWA_ERR_UNSUPPORTED, "too many key blocks for one launch");
   COWA_TRY(check_device());
-  return hip_status(cowa::launch_bwd_main(*p, cowa::sched_view(s), q, k, v, lse, d_o, dk, dv, dq_acc, dsum,
+  return hip_status(cowa::launch_bwd_main(*p, cowa::sched_view(s), q, k, v, lse, d_o, dk, dv, dsum,
                                           static_cast<hipStream_t>(stream)),
-                    "backward main launch");
+                    "backward dK/dV launch");
 }
 
-cowa_status cowa_bwd_finish(const cowa_params* p, void* dq, void* workspace, size_t ws_bytes, void* stream) {
-  float *dq_acc, *dsum;
-  COWA_TRY(check_bwd(p, ws_bytes, workspace, &dq_acc, &dsum));
+cowa_status cowa_bwd_dq(const cowa_params* p, const cowa_schedule_t* s, const void* q, const void* k, const void* v,
+                        const float* lse, const void* d_o, void* dq, void* workspace, size_t ws_bytes,
+                        void* stream) {
+  float* dsum;
+  COWA_TRY(check_bwd(p, ws_bytes, workspace, &dsum));
+  COWA_TRY(check_schedule(p, s));
   if (p->batch == 0) return COWA_OK;
+  COWA_TRY(check_qkv_lse_do(q, k, v, lse, d_o));
   COWA_TRY(check_tensor(dq, "dq", 16));
+  if ((int64_t)s->n_qt * p->h_q * p->batch >= (int64_t(1) << 31))
+    return fail(COWA_ERR_UNSUPPORTED, "too many query blocks for one launch");
   COWA_TRY(check_device());
-  return hip_status(cowa::launch_bwd_finish(*p, dq_acc, dq, static_cast<hipStream_t>(stream)),
-                    "backward finish launch");
+  return hip_status(cowa::launch_bwd_dq(*p, cowa::sched_view(s), q, k, v, lse, d_o, dq, dsum,
+                                        static_cast<hipStream_t>(stream)),
+                    "backward dQ launch");
 }
 
 cowa_status cowa_bwd(const cowa_params* p, const cowa_schedule_t* s, const void* q, const void* k, const void* v,
                      const void* o, const float* lse, const void* d_o, void* dq, void* dk, void* dv, void* workspace,
                      size_t ws_bytes, void* stream) {
-  float *dq_acc, *dsum;
-  COWA_TRY(check_bwd(p, ws_bytes, workspace, &dq_acc, &dsum));
+  float* dsum;
+  COWA_TRY(check_bwd(p, ws_bytes, workspace, &dsum));
   COWA_TRY(check_schedule(p, s));
   if (p->batch == 0) return COWA_OK;
   const void* ptrs[] = {q, k, v, o, d_o, dq, dk, dv};
@@ -327,7 +336,7 @@ cowa_status cowa_bwd(const cowa_params* p, const cowa_schedule_t* s, const void*
   COWA_TRY(check_tensor(lse, "lse", 4));
   COWA_TRY(cowa_bwd_prepare(p, o, d_o, workspace, ws_bytes, stream));
   COWA_TRY(cowa_bwd_main(p, s, q, k, v, lse, d_o, dk, dv, workspace, ws_bytes, stream));
-  return cowa_bwd_finish(p, dq, workspace, ws_bytes, stream);
+  return cowa_bwd_dq(p, s, q, k, v, lse, d_o, dq, workspace, ws_bytes, stream);
 }
 
 static cowa_status check_decode_params(const cowa_decode_params* p) {

@@ -25,64 +25,17 @@
 // Finally O = O / l and LSE = (m + log2 l) ln 2 (natural log).
 #include "internal.h"
 #include "window_rule.h"
+#include "mfma_tiles.h"
 
 namespace cowa {
 namespace {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void;
-typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-
-constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kLn2 = 0.6931471805599453f;
-
-// Workgroups id, id + 8, id + 16, ... land on the same XCD (round-robin
-// dispatch over the 8 XCDs).  Hand each XCD whole chunks of 8 consecutive work
-// items so that items sharing K/V blocks share that XCD's L2.
-__device__ inline int xcd_remap(int id, int total) {
-  const int full = (total / 64) * 64;
-  if (id >= full) return id;
-  const int xcd = id & 7, slot = id >> 3;
-  const int chunk = (slot >> 3) * 8 + xcd;
-  return chunk * 8 + (slot & 7);
-}
-
-template <int D, int BK>
-struct Tile {
-  static constexpr int CH = D / 8;                 // 16-byte chunks per row
-  static constexpr int BYTES = BK * D * 2;         // one K or V block
-  static constexpr int LOADS = BYTES / 1024;       // 1 KB direct loads per block
-  // byte offset of (row, 16-byte chunk) inside a swizzled block
-  __device__ static inline int off(int row, int chunk) { return row * (D * 2) + ((chunk ^ (row % CH)) << 4); }
-};
-
-// Copy rows [k_first, k_first + BK) of a [n_k][D] bf16 matrix into a swizzled
-// LDS block; rows past n_k repeat the last row (they are masked later).
-template <int D, int BK>
-__device__ inline void load_block(const __bf16* base, int64_t k_first, int n_k, unsigned char* lds_block, int wave,
-                                  int nw, int lane) {
-  using T = Tile<D, BK>;
-  for (int n = wave; n < T::LOADS; n += nw) {
-    const int flat = n * 64 + lane;           // 16-byte unit index = LDS position
-    const int row = flat / T::CH, slot = flat % T::CH;
-    const int chunk = slot ^ (row % T::CH);   // global chunk stored at that position
-    int64_t kp = k_first + row;
-    if (kp >= n_k) kp = n_k - 1;
-    const __bf16* src = base + kp * D + chunk * 8;
-    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src),
-                                     (lds_void*)(lds_block + n * 1024), 16, 0, 0);
-  }
-}
 
 template <int D, int BQ, int BK, int NQW>
 __global__ void __launch_bounds__(512) fwd_bf16_kernel(cowa_params p, SchedView sv, int hpw, int n_hgroups,
                                                        const __bf16* __restrict__ q, const __bf16* __restrict__ k,
                                                        const __bf16* __restrict__ v, __bf16* __restrict__ o,
                                                        float* __restrict__ lse) {
-  using T = Tile<D, BK>;
+  using T = SwzTile<D, BK>;
   constexpr int NTQ = NQW / 16;           // query tiles per wave
   constexpr int BKC = BK > 64 ? 64 : BK;   // keys per softmax step (a KV block is 1 or 2 steps)
   constexpr int MTK = BKC / 16;           // key tiles of S^T
@@ -117,8 +70,8 @@ __global__ void __launch_bounds__(512) fwd_bf16_kernel(cowa_params p, SchedView 
   // buffer s: K at smem + 2 s BYTES, V right after it
   if (e0 < e1) {
     const int64_t kf = (int64_t)(sv.fwd_ent[e0] >> 1) * BK;
-    load_block<D, BK>(kbase, kf, p.n_k, smem, wave, nw, lane);
-    load_block<D, BK>(vbase, kf, p.n_k, smem + T::BYTES, wave, nw, lane);
+    load_tile<D, BK>(kbase, kf, p.n_k, smem, wave, nw, lane);
+    load_tile<D, BK>(vbase, kf, p.n_k, smem + T::BYTES, wave, nw, lane);
   }
 
   // Q^T fragments (B operand): query column nt*16 + lr, d = ks*32 + 8*lg + 0..7
@@ -157,8 +110,8 @@ __global__ void __launch_bounds__(512) fwd_bf16_kernel(cowa_params p, SchedView 
     if (e + 1 < e1) {  // prefetch the next block into the other buffer
       const int64_t kf = (int64_t)(sv.fwd_ent[e + 1] >> 1) * BK;
       unsigned char* nb = smem + (buf ^ 1) * 2 * T::BYTES;
-      load_block<D, BK>(kbase, kf, p.n_k, nb, wave, nw, lane);
-      load_block<D, BK>(vbase, kf, p.n_k, nb + T::BYTES, wave, nw, lane);
+      load_tile<D, BK>(kbase, kf, p.n_k, nb, wave, nw, lane);
+      load_tile<D, BK>(vbase, kf, p.n_k, nb + T::BYTES, wave, nw, lane);
     }
     const unsigned char* Kt = smem + buf * 2 * T::BYTES;
     const unsigned char* Vt = Kt + T::BYTES;
@@ -234,8 +187,6 @@ __global__ void __launch_bounds__(512) fwd_bf16_kernel(cowa_params p, SchedView 
       // O^T += V_j^T P^T.  k-slot t of step ks is key 32ks + 4lg + t (t < 4) or
       // 32ks + 16 + 4lg + (t - 4); the transposing read gives lane lr the column
       // d = md*16 + lr of four keys, supplied by lanes 4*t + (lr / 4) of its group.
-      const int sup_key = 4 * lg + (lr >> 2);
-      const int sup_dq = lr & 3;
   #pragma unroll
       for (int ks = 0; ks < KSK; ++ks) {
         bf16x8 pb[NTQ];
@@ -246,20 +197,11 @@ __global__ void __launch_bounds__(512) fwd_bf16_kernel(cowa_params p, SchedView 
             pb[nt][rr] = (__bf16)sacc[2 * ks][nt][rr];
             pb[nt][4 + rr] = (__bf16)sacc[2 * ks + 1][nt][rr];
           }
-        const int row0 = kc + ks * 32 + sup_key, row1 = row0 + 16;
   #pragma unroll
         for (int md = 0; md < MTD; ++md) {
-          const int byte = (md * 16 + 4 * sup_dq) * 2;  // within the row
-          const int chunk = byte >> 4, half = byte & 15;
-          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_i16x4*)(Vt + T::off(row0, chunk) + half));
-          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_i16x4*)(Vt + T::off(row1, chunk) + half));
-          const bf16x4 lob = __builtin_bit_cast(bf16x4, lo), hib = __builtin_bit_cast(bf16x4, hi);
-          const bf16x8 a = {lob[0], lob[1], lob[2], lob[3], hib[0], hib[1], hib[2], hib[3]};
+          const bf16x8 a = read_tr8<D, BK>(Vt, kc + ks * 32, md * 16, lr, lg);
   #pragma unroll
-          for (int nt = 0; nt < NTQ; ++nt)
-            oacc[md][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[nt], oacc[md][nt], 0, 0, 0);
+          for (int nt = 0; nt < NTQ; ++nt) oacc[md][nt] = mfma16(a, pb[nt], oacc[md][nt]);
         }
       }
     }
@@ -293,7 +235,7 @@ __global__ void __launch_bounds__(512) fwd_bf16_kernel(cowa_params p, SchedView 
 template <int D, int BQ, int BK, int NQW = 32>
 hipError_t launch_cfg(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
                       void* o, float* lse, hipStream_t stream) {
-  constexpr int LDS = 4 * Tile<D, BK>::BYTES;
+  constexpr int LDS = 4 * SwzTile<D, BK>::BYTES;
   static_assert(LDS <= 160 * 1024, "LDS budget");
   auto kern = fwd_bf16_kernel<D, BQ, BK, NQW>;
   static bool attr_set = false;

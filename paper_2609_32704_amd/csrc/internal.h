@@ -41,14 +41,14 @@ bool bwd_bf16_supported(int head_dim, int tile_q, int tile_k);
 hipError_t launch_fwd_bf16(const cowa_params& p, const SchedView& sv, const void* q, const void* k,
                            const void* v, void* o, float* lse, hipStream_t stream);
 
-// Backward stages (Alg. 2): D = rowsum(O * dO) and a zeroed dQ accumulator; the
-// main pass (dK, dV written, dQ accumulated); the dQ conversion to bf16.
-hipError_t launch_bwd_prepare(const cowa_params& p, const void* o, const void* d_o, float* dq_acc, float* dsum,
+// Backward stages (Alg. 2): D = rowsum(O * dO); the dK/dV pass; the dQ pass.
+hipError_t launch_bwd_prepare(const cowa_params& p, const void* o, const void* d_o, float* dsum,
                               hipStream_t stream);
 hipError_t launch_bwd_main(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
-                           const float* lse, const void* d_o, void* dk, void* dv, float* dq_acc, const float* dsum,
+                           const float* lse, const void* d_o, void* dk, void* dv, const float* dsum,
                            hipStream_t stream);
-hipError_t launch_bwd_finish(const cowa_params& p, const float* dq_acc, void* dq, hipStream_t stream);
+hipError_t launch_bwd_dq(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
+                         const float* lse, const void* d_o, void* dq, const float* dsum, hipStream_t stream);
 
 bool decode_supported(int head_dim, int group);
 size_t decode_workspace_bytes(const cowa_decode_params& p);
