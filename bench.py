@@ -122,6 +122,8 @@ def main():
     ap.add_argument("--dense-iters", type=int, default=2)
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--only", choices=["all", "train", "decode", "copy"], default="all",
+                    help="profiling aid: run only part of the step (the JSON line is printed for 'all' only)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on exactly one GPU: the CoWA path shards by KV head with no exchange, "
@@ -145,12 +147,26 @@ def main():
             out[s].copy_(torch.randn(shape[1:], generator=gen, device=dev, dtype=torch.float32))
         return out
 
+    if args.only == "copy":
+        # plain device copy of a known size: the reference for HBM byte counters
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst2 = torch.empty_like(src)
+        for _ in range(3):
+            dst2.copy_(src)
+        torch.cuda.synchronize()
+        log("copied 3 x 1 GiB")
+        return
+
+    do_train = args.only in ("all", "train")
+    do_decode = args.only in ("all", "decode")
     T = TRAIN
     log("allocating training inputs")
-    q = randn((T["batch"], T["h_q"], T["n"], T["d"]))
-    k = randn((T["batch"], T["h_k"], T["n"], T["d"]))
-    v = randn((T["batch"], T["h_k"], T["n"], T["d"]))
-    do = randn((T["batch"], T["h_q"], T["n"], T["d"]))
+    tq = (T["batch"], T["h_q"], T["n"], T["d"]) if do_train else (1, 1, 1, T["d"])
+    tk = (T["batch"], T["h_k"], T["n"], T["d"]) if do_train else (1, 1, 1, T["d"])
+    q = randn(tq)
+    k = randn(tk)
+    v = randn(tk)
+    do = randn(tq)
     o = torch.empty_like(q)
     lse = torch.empty((T["batch"], T["h_q"], T["n"]), dtype=torch.float32, device=dev)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
@@ -170,8 +186,8 @@ def main():
     D = DECODE
     log("allocating decode inputs (2 x 17 GB KV cache)")
     dq_in = randn((D["batch"], D["h_q"], D["d"]))
-    kc = randn((D["batch"], D["h_k"], D["n"], D["d"]))
-    vc = randn((D["batch"], D["h_k"], D["n"], D["d"]))
+    kc = randn((D["batch"], D["h_k"], D["n"], D["d"]) if do_decode else (1, 1, 1, D["d"]))
+    vc = randn((D["batch"], D["h_k"], D["n"], D["d"]) if do_decode else (1, 1, 1, D["d"]))
     seqlens_host = [D["n"]] * D["batch"]
     seqlens = torch.tensor(seqlens_host, dtype=torch.int32, device=dev)
     dpar = cowa.make_decode_params(D["batch"], D["h_q"], D["h_k"], D["d"], D["n"], D["w_sink"], D["w_near"])
@@ -185,6 +201,13 @@ def main():
 
     def step(evs):
         evs[0].record()
+        if not do_train:
+            for e in evs[1:6]:
+                e.record()
+            _abi.cowa_decode(dpar, dq_in.data_ptr(), kc.data_ptr(), vc.data_ptr(), seqlens.data_ptr(),
+                             od.data_ptr(), lsed.data_ptr(), dws.data_ptr(), dws.numel(), stream)
+            evs[6].record()
+            return
         _abi.cowa_windows(p)
         _abi.cowa_schedule(sched.s, stream)
         evs[1].record()
@@ -198,8 +221,9 @@ def main():
         _abi.cowa_bwd_dq(p, sched.s, q.data_ptr(), k.data_ptr(), v.data_ptr(), lse.data_ptr(), do.data_ptr(),
                          dq.data_ptr(), ws.data_ptr(), ws_bytes, stream)
         evs[5].record()
-        _abi.cowa_decode(dpar, dq_in.data_ptr(), kc.data_ptr(), vc.data_ptr(), seqlens.data_ptr(), od.data_ptr(),
-                         lsed.data_ptr(), dws.data_ptr(), dws.numel(), stream)
+        if do_decode:
+            _abi.cowa_decode(dpar, dq_in.data_ptr(), kc.data_ptr(), vc.data_ptr(), seqlens.data_ptr(),
+                             od.data_ptr(), lsed.data_ptr(), dws.data_ptr(), dws.numel(), stream)
         evs[6].record()
 
     def new_events():
@@ -222,6 +246,9 @@ def main():
         for idx, n in enumerate(names):
             per[n] += evs[idx].elapsed_time(evs[idx + 1])
     per = {n: per[n] / args.steps for n in names}
+    if args.only != "all":
+        log("per-kernel ms:", {n: round(x, 3) for n, x in per.items()})
+        return
     bwd_ms = per["bwd_prepare"] + per["bwd_main"] + per["bwd_dq"]
     train_ms = per["schedule"] + per["fwd"] + bwd_ms
     value = (fwd_flops + bwd_flops) / (train_ms * 1e-3) / 1e12
