@@ -300,6 +300,9 @@ cowa_status cowa_bwd_main(const cowa_params* p, const cowa_schedule_t* s, const 
   COWA_TRY(check_tensor(dv, "dv", 16));
   if ((int64_t)s->n_kt * p->h_k * p->batch >= (int64_t(1) << 31))
     return fail(COWA_ERR_UNSUPPORTED, "too many key blocks for one launch");
+  if (s->n_qt > cowa::bwd_main_max_qblocks(p->head_dim, p->tile_k))
+    return fail(COWA_ERR_UNSUPPORTED, "backward dK/dV pass supports at most %d query blocks (got %d)",
+                cowa::bwd_main_max_qblocks(p->head_dim, p->tile_k), s->n_qt);
   COWA_TRY(check_device());
   return hip_status(cowa::launch_bwd_main(*p, cowa::sched_view(s), q, k, v, lse, d_o, dk, dv, dsum,
                                           static_cast<hipStream_t>(stream)),

@@ -64,12 +64,20 @@ struct BwdCfg {
   static constexpr int KSD = D / 32;      // k-steps over d
   static constexpr int MD = D / 16;       // d tiles
   static constexpr int KSQ = BQ / 32;     // k-steps over queries
-  static constexpr int KSK = BK / 32;     // k-steps over keys
   using QT = SwzTile<D, BQ>;              // Q or dO rows of one step
-  static constexpr int ROWV = 2 * BQ * 4; // per-step row values: LSE [BQ], then D [BQ]
-  static constexpr int STAGE = 2 * QT::BYTES + ROWV;     // Q, dO and row values of one step
-  static constexpr int OUT_BYTES = 2 * BK * (D + 8) * 2;  // dK, dV staging at the end
-  static constexpr int LDS_BYTES = 2 * STAGE > OUT_BYTES ? 2 * STAGE : OUT_BYTES;
+  static constexpr int ROWV = 2 * BQ * 4; // per-step row values: base-2 LSE [BQ], then D [BQ]
+  // LDS: Q of stages 0, 1; dO of stages 0, 1; row values of stages 0, 1
+  static constexpr int Q_OFF0 = 0, Q_OFF1 = QT::BYTES, DO_OFF0 = 2 * QT::BYTES, DO_OFF1 = 3 * QT::BYTES;
+  static constexpr int RV_OFF0 = 4 * QT::BYTES, RV_OFF1 = 4 * QT::BYTES + ROWV;
+  static constexpr int MAIN_BYTES = 4 * QT::BYTES + 2 * ROWV;  // then the column's entry lists
+  static constexpr int OUT_BYTES = 2 * BK * (D + 8) * 2;        // dK, dV staging at the end
+  static constexpr int LDS_MAX = 160 * 1024;
+  // LDS for a schedule with n_qt query blocks
+  static int lds_bytes(int n_qt) {
+    const int main = MAIN_BYTES + 4 * n_qt;
+    return main > OUT_BYTES ? main : OUT_BYTES;
+  }
+  static int max_qblocks() { return (LDS_MAX - MAIN_BYTES) / 4; }
 };
 
 template <int D, int BK>
@@ -89,54 +97,93 @@ __global__ void __launch_bounds__(256) bwd_main(cowa_params p, SchedView sv, con
   const int G = p.h_q / p.h_k;
   const Geo32 g = geo32(make_geo(p.n_q, p.n_k, p.w_sink, p.w_near, p.tile_q, BK, p.h_k_offset + hk, p.h_k_total));
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int nw = blockDim.x >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int64_t k_first = (int64_t)j * BK;
   const __bf16* kbase = k + ((int64_t)b * p.h_k + hk) * p.n_k * D;
   const __bf16* vbase = v + ((int64_t)b * p.h_k + hk) * p.n_k * D;
 
-  // the step list: every QO head of the group x every QO block of I(j) x 64-row sub-steps
+  // The steps: every QO head of the group x every QO block of I(j) x 64-row
+  // sub-blocks.  Full blocks are taken first, then partial ones, so that each
+  // of the two step loops below is straight-line code (the partial loop adds
+  // the element mask).  The column's entries are split once into two lists in
+  // LDS: full entries from the front, partial entries from the back.
   const int col = hk * sv.n_kt + j;
   const int e0 = sv.bwd_col_ptr[col], e1 = sv.bwd_col_ptr[col + 1];
+  const int n_ent = e1 - e0;
+  const int cap = sv.n_qt;  // list capacity (entries of one column)
+  uint32_t* list = reinterpret_cast<uint32_t*>(smem + C::MAIN_BYTES);
+  int n_full = 0;
+  for (int c0 = 0; c0 < n_ent; c0 += 64) {  // every wave builds the same counts; wave 0 writes
+    const bool in = c0 + lane < n_ent;
+    const uint32_t ent = in ? sv.bwd_ent[e0 + c0 + lane] : 0u;
+    const uint64_t full = __ballot(in && !(ent & 1u));
+    const uint64_t part = __ballot(in && (ent & 1u));
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    const int n_part_before = c0 - n_full;
+    if (wave == 0 && in) {
+      if (ent & 1u)
+        list[cap - 1 - (n_part_before + __popcll(part & below))] = ent;
+      else
+        list[n_full + __popcll(full & below)] = ent;
+    }
+    n_full += __popcll(full);
+  }
+  const int n_part = n_ent - n_full;
   const int subs = p.tile_q / C::BQ;
-  const int per_head = (e1 - e0) * subs;
-  const int n_steps = G * per_head;
-  auto step_rows = [&](int t, int& h, int64_t& q0, bool& partial) {
-    const int hh = t / per_head, rem = t % per_head;
-    const uint32_t ent = sv.bwd_ent[e0 + rem / subs];
-    h = hk * G + hh;
-    q0 = (int64_t)(ent >> 1) * p.tile_q + (rem % subs) * C::BQ;
-    partial = ent & 1u;
-  };
-  // Q and dO rows of step t go global -> LDS directly; the step's LSE and D
-  // values go through registers of the last wave (rows past n_q: LSE = -inf, D = 0)
-  auto stage_step = [&](int t, unsigned char* st, float& lv, float& dv2) {
-    int h;
-    int64_t q0;
-    bool partial;
-    step_rows(t, h, q0, partial);
-    const int64_t row_base = ((int64_t)b * p.h_q + h) * p.n_q;
-    load_tile<D, C::BQ>(q + row_base * D, q0, p.n_q, st, wave, nw, lane);
-    load_tile<D, C::BQ>(d_o + row_base * D, q0, p.n_q, st + C::QT::BYTES, wave, nw, lane);
-    if (wave == nw - 1) {
-      const int64_t r = q0 + lane;
-      lv = r < p.n_q ? lse[row_base + r] : -INFINITY;
-      dv2 = r < p.n_q ? dsum[row_base + r] : 0.f;
+  const int steps_full = G * n_full * subs, n_steps = G * n_ent * subs;
+  // cursor (phase: 0 full / 1 partial, QO head, list index, sub-block)
+  int c_ph = n_full > 0 ? 0 : 1, c_hh = 0, c_k = 0, c_sub = 0;  // step being computed
+  int n_ph = c_ph, n_hh = 0, n_k = 0, n_sub = 0;               // step being staged
+  auto advance = [&](int& ph, int& hh, int& kk, int& sub) {
+    if (++sub == subs) {
+      sub = 0;
+      if (++kk == (ph == 0 ? n_full : n_part)) {
+        kk = 0;
+        if (++hh == G) {
+          hh = 0;
+          ++ph;
+          if (ph == 1 && n_part == 0) ph = 2;  // past the end
+        }
+      }
     }
   };
-  auto store_rowv = [&](unsigned char* st, float lv, float dv2) {
-    if (wave == nw - 1) {
-      float* rv = reinterpret_cast<float*>(st + 2 * C::QT::BYTES);
-      rv[lane] = lv;
-      rv[C::BQ + lane] = dv2;
-    }
+  // list entry of a cursor; a cursor past the end names the first entry
+  auto entry_of = [&](int ph, int kk) -> uint32_t {
+    const int idx = ph == 0 ? kk : (ph == 1 ? cap - 1 - kk : (n_full > 0 ? 0 : cap - 1));
+    return __builtin_amdgcn_readfirstlane(list[idx]);
   };
 
-  float nlv = 0.f, ndv = 0.f;  // row values of the step being staged
+  // Q and dO rows of a step go global -> LDS directly; its LSE (as base 2; a
+  // row without keys or past n_q gets +inf, so P = 0) and D values go through
+  // registers (every wave loads and stores the same 64 values, which keeps
+  // the step free of branches).  A cursor past the last step stages a copy of
+  // the last head's rows, never read.
+  float st_l2 = 0.f, st_dd = 0.f;
+  auto stage = [&](uint32_t ent, int hh, int sub, int q_off, int do_off) {
+    hh = hh < G ? hh : G - 1;
+    const int q0 = (int)(ent >> 1) * p.tile_q + sub * C::BQ;
+    const int64_t row_base = ((int64_t)b * p.h_q + hk * G + hh) * p.n_q;
+    load_tile<D, C::BQ, 4>(q + row_base * D, q0, p.n_q, smem + q_off, wave, lane);
+    load_tile<D, C::BQ, 4>(d_o + row_base * D, q0, p.n_q, smem + do_off, wave, lane);
+    const int r = q0 + lane;
+    const int rc = r < p.n_q ? r : p.n_q - 1;
+    const float lv = lse[row_base + rc], dv0 = dsum[row_base + rc];
+    st_l2 = (r < p.n_q && lv != -INFINITY) ? lv * kLog2e : INFINITY;
+    st_dd = r < p.n_q ? dv0 : 0.f;
+  };
+  auto store_rowv = [&](int rv_off) {
+    float* rv = reinterpret_cast<float*>(smem + rv_off);
+    rv[lane] = st_l2;
+    rv[C::BQ + lane] = st_dd;
+  };
+
+  __syncthreads();  // the entry lists are in LDS
   if (n_steps > 0) {
-    stage_step(0, smem, nlv, ndv);
-    store_rowv(smem, nlv, ndv);
+    stage(entry_of(n_ph, n_k), n_hh, n_sub, C::Q_OFF0, C::DO_OFF0);
+    store_rowv(C::RV_OFF0);
+    advance(n_ph, n_hh, n_k, n_sub);
   }
 
   // K and V rows of this wave's keys as B fragments: key nt*16 + lr, d = ks*32 + 8*lg + 0..7
@@ -144,14 +191,14 @@ __global__ void __launch_bounds__(256) bwd_main(cowa_params p, SchedView sv, con
 #pragma unroll
   for (int nt = 0; nt < C::NTK; ++nt) {
     int64_t kp = k_first + wave * C::NKW + nt * 16 + lr;
-    if (kp >= p.n_k) kp = p.n_k - 1;  // masked below: such keys are in partial blocks only
+    if (kp >= p.n_k) kp = p.n_k - 1;  // masked: such keys are in partial blocks only
 #pragma unroll
     for (int ks = 0; ks < C::KSD; ++ks) {
       kf[nt][ks] = *reinterpret_cast<const bf16x8*>(kbase + kp * D + ks * 32 + 8 * lg);
       vf[nt][ks] = *reinterpret_cast<const bf16x8*>(vbase + kp * D + ks * 32 + 8 * lg);
     }
   }
-  f32x4 dka[C::MD][C::NTK], dva[C::MD][C::NTK];  // dK^T, dV^T: rows d, columns keys
+  f32x4 dka[C::MD][C::NTK], dva[C::MD][C::NTK];  // dK^T / scale, dV^T: rows d, columns keys
 #pragma unroll
   for (int md = 0; md < C::MD; ++md)
 #pragma unroll
@@ -159,100 +206,124 @@ __global__ void __launch_bounds__(256) bwd_main(cowa_params p, SchedView sv, con
       dka[md][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
       dva[md][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
+  // per-lane LDS offsets of the row-fragment and transposing reads
+  int offr[C::KSD], offt[C::MD];
+#pragma unroll
+  for (int ks = 0; ks < C::KSD; ++ks) offr[ks] = row8_off<D>(lr, lg, ks);
+#pragma unroll
+  for (int md = 0; md < C::MD; ++md) offt[md] = tr8_off<D>(lr, lg, md);
   const float c = p.softmax_scale * kLog2e;
-  const float scale = p.softmax_scale;
+  const int k0 = (int)k_first + wave * C::NKW + lr;  // key of column nt*16 + lr
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
-  for (int t = 0; t < n_steps; ++t) {
-    unsigned char* st = smem + (t & 1) * C::STAGE;
-    unsigned char* nst = smem + ((t + 1) & 1) * C::STAGE;
-    if (t + 1 < n_steps) stage_step(t + 1, nst, nlv, ndv);
-    int h;
-    int64_t q0;
-    bool partial;
-    step_rows(t, h, q0, partial);
-    const unsigned char* qs = st;
-    const unsigned char* dos = st + C::QT::BYTES;
-    const float* rowv = reinterpret_cast<const float*>(st + 2 * C::QT::BYTES);
-
-    // S = Q K^T and dP = dO V^T: rows q = mt*16 + 4*lg + r, column key = nt*16 + lr
-    f32x4 sacc[C::MTQ][C::NTK], pacc[C::MTQ][C::NTK];
-#pragma unroll
-    for (int mt = 0; mt < C::MTQ; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < C::NTK; ++nt) {
-        sacc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        pacc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      }
+  // One step on stage st (0 or 1):
+  //   S = Q K^T, dP = dO V^T, P = exp(S - LSE), dS = P (dP - D),
+  //   dV^T += dO^T P, dK^T += Q^T dS (the softmax scale is applied to dK at the end).
+  // The 64 rows are taken in two halves of 32 (one k-step of the dV/dK
+  // products), and the phases are ordered so that the matrix cores always have
+  // independent work while the vector units run a softmax:
+  //   S/dP(0) | S/dP(1) + softmax(0) | dV/dK(0) + softmax(1) | dV/dK(1).
+  // Scheduling fences keep the phases apart (and the live registers bounded).
+  f32x4 sacc[C::MTQ][C::NTK], pacc[C::MTQ][C::NTK];  // rows q = mt*16 + 4*lg + r, column key = nt*16 + lr
+  bf16x8 pb[C::KSQ][C::NTK], sb[C::KSQ][C::NTK];     // P and dS as B operands, k-slots = queries of a half
+  auto sdp_half = [&](const unsigned char* qs, const unsigned char* dos, int hf) {
 #pragma unroll
     for (int ks = 0; ks < C::KSD; ++ks)
 #pragma unroll
-      for (int mt = 0; mt < C::MTQ; ++mt) {
-        const bf16x8 aq = read_row8<D, C::BQ>(qs, mt * 16 + lr, ks * 4 + lg);
-        const bf16x8 ag = read_row8<D, C::BQ>(dos, mt * 16 + lr, ks * 4 + lg);
+      for (int mt = 2 * hf; mt < 2 * hf + 2; ++mt) {
+        const bf16x8 aq = ld_row8(qs + offr[ks] + mt * 16 * D * 2);
+        const bf16x8 ag = ld_row8(dos + offr[ks] + mt * 16 * D * 2);
 #pragma unroll
         for (int nt = 0; nt < C::NTK; ++nt) {
-          sacc[mt][nt] = mfma16(aq, kf[nt][ks], sacc[mt][nt]);
-          pacc[mt][nt] = mfma16(ag, vf[nt][ks], pacc[mt][nt]);
+          sacc[mt][nt] = mfma16(aq, kf[nt][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sacc[mt][nt]);
+          pacc[mt][nt] = mfma16(ag, vf[nt][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : pacc[mt][nt]);
         }
       }
-
-    // P = exp(S - LSE) and scale * dS = scale * P (dP - D); masked pairs get P = 0
-    // through an additive -inf in the exponent (the value read keeps the MFMA
-    // result ordering).  A row whose LSE is -inf has no legal key: P = 0.
-    const int64_t qrow = q0 + 4 * lg;  // + mt*16 + r
-    const int k0 = (int)k_first + wave * C::NKW + lr;
+  };
+  // P and dS of a half, rounded to bf16 in the B-operand layout: k-slot 4 i + t
+  // is query row (2 hf + i) * 16 + 4 lg + t.  In a partial block the masked
+  // pairs get P = 0 through an additive -inf in the exponent (an update that
+  // reads the MFMA result).
+  auto softmax_half = [&](const float* rowv, int hf, bool masked, int q0) {
+    const int qi0 = q0 + 4 * lg;
 #pragma unroll
-    for (int mt = 0; mt < C::MTQ; ++mt) {
-      const float4 lv = *reinterpret_cast<const float4*>(rowv + mt * 16 + 4 * lg);
-      const float4 dv4 = *reinterpret_cast<const float4*>(rowv + C::BQ + mt * 16 + 4 * lg);
-      const float lsev[4] = {lv.x, lv.y, lv.z, lv.w}, dd[4] = {dv4.x, dv4.y, dv4.z, dv4.w};
+    for (int i = 0; i < 2; ++i) {
+      const int mt = 2 * hf + i;
+      const float4 l4 = *reinterpret_cast<const float4*>(rowv + mt * 16 + 4 * lg);
+      const float4 d4 = *reinterpret_cast<const float4*>(rowv + C::BQ + mt * 16 + 4 * lg);
+      const float l2[4] = {l4.x, l4.y, l4.z, l4.w}, dd[4] = {d4.x, d4.y, d4.z, d4.w};
 #pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const float l2 = lsev[rr] == -INFINITY ? INFINITY : lsev[rr] * kLog2e;
-        const int qi = (int)qrow + mt * 16 + rr;
+      for (int rr = 0; rr < 4; ++rr)
 #pragma unroll
         for (int nt = 0; nt < C::NTK; ++nt) {
-          const float bias = (!partial || legal32(g, qi, k0 + nt * 16)) ? 0.f : -INFINITY;
-          const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[mt][nt][rr], c, -l2) + bias);
-          sacc[mt][nt][rr] = pv;
-          pacc[mt][nt][rr] = scale * pv * (pacc[mt][nt][rr] - dd[rr]);
+          float x = fmaf(sacc[mt][nt][rr], c, -l2[rr]);
+          if (masked) x += legal32(g, qi0 + mt * 16 + rr, k0 + nt * 16) ? 0.f : -INFINITY;
+          const float pv = __builtin_amdgcn_exp2f(x);
+          pb[hf][nt][4 * i + rr] = (__bf16)pv;
+          sb[hf][nt][4 * i + rr] = (__bf16)(pv * (pacc[mt][nt][rr] - dd[rr]));
         }
+    }
+  };
+  auto dvdk_half = [&](const unsigned char* qs, const unsigned char* dos, int hf) {
+#pragma unroll
+    for (int md = 0; md < C::MD; ++md) {
+      const bf16x8 ag = ld_tr8(dos + offt[md] + hf * 32 * D * 2, D * 2);
+      const bf16x8 aq = ld_tr8(qs + offt[md] + hf * 32 * D * 2, D * 2);
+#pragma unroll
+      for (int nt = 0; nt < C::NTK; ++nt) {
+        dva[md][nt] = mfma16(ag, pb[hf][nt], dva[md][nt]);
+        dka[md][nt] = mfma16(aq, sb[hf][nt], dka[md][nt]);
       }
     }
+  };
 
-    // dV^T += dO^T P and dK^T += Q^T (scale dS): k-slots are queries 32ks + 4lg + t, 32ks + 16 + 4lg + t
-#pragma unroll
-    for (int ks = 0; ks < C::KSQ; ++ks) {
-      bf16x8 pb[C::NTK], sb[C::NTK];
-#pragma unroll
-      for (int nt = 0; nt < C::NTK; ++nt)
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          pb[nt][rr] = (__bf16)sacc[2 * ks][nt][rr];
-          pb[nt][4 + rr] = (__bf16)sacc[2 * ks + 1][nt][rr];
-          sb[nt][rr] = (__bf16)pacc[2 * ks][nt][rr];
-          sb[nt][4 + rr] = (__bf16)pacc[2 * ks + 1][nt][rr];
-        }
-#pragma unroll
-      for (int md = 0; md < C::MD; ++md) {
-        const bf16x8 ag = read_tr8<D, C::BQ>(dos, ks * 32, md * 16, lr, lg);
-        const bf16x8 aq = read_tr8<D, C::BQ>(qs, ks * 32, md * 16, lr, lg);
-#pragma unroll
-        for (int nt = 0; nt < C::NTK; ++nt) {
-          dva[md][nt] = mfma16(ag, pb[nt], dva[md][nt]);
-          dka[md][nt] = mfma16(aq, sb[nt], dka[md][nt]);
-        }
-      }
-    }
+  auto step = [&](int t, bool masked) {
+    const int st = t & 1;
+    const unsigned char* qs = smem + (st ? C::Q_OFF1 : C::Q_OFF0);
+    const unsigned char* dos = smem + (st ? C::DO_OFF1 : C::DO_OFF0);
+    const float* rowv = reinterpret_cast<const float*>(smem + (st ? C::RV_OFF1 : C::RV_OFF0));
+    const int q0 = (int)(entry_of(c_ph, c_k) >> 1) * p.tile_q + c_sub * C::BQ;
+    stage(entry_of(n_ph, n_k), n_hh, n_sub, st ? C::Q_OFF0 : C::Q_OFF1, st ? C::DO_OFF0 : C::DO_OFF1);
 
-    if (t + 1 < n_steps) store_rowv(nst, nlv, ndv);
+    sdp_half(qs, dos, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    sdp_half(qs, dos, 1);
+    softmax_half(rowv, 0, masked, q0);
+    __builtin_amdgcn_sched_barrier(0);
+    dvdk_half(qs, dos, 0);
+    softmax_half(rowv, 1, masked, q0);
+    __builtin_amdgcn_sched_barrier(0);
+    dvdk_half(qs, dos, 1);
+
+    store_rowv(st ? C::RV_OFF0 : C::RV_OFF1);
+    // Register placement (the library builds this file with MFMA results in
+    // VGPRs): the dK/dV accumulators stay in VGPRs and the K/V fragments in
+    // AGPRs, which the MFMAs read directly as B operands.  These empty
+    // statements emit nothing; they only pin the register class across steps
+    // (otherwise the allocator shuffles values between the two files).
+#pragma unroll
+    for (int md = 0; md < C::MD; ++md)
+#pragma unroll
+      for (int nt = 0; nt < C::NTK; ++nt) asm volatile("" : "+v"(dka[md][nt]), "+v"(dva[md][nt]));
+#pragma unroll
+    for (int nt = 0; nt < C::NTK; ++nt)
+#pragma unroll
+      for (int ks = 0; ks < C::KSD; ++ks) asm volatile("" : "+a"(kf[nt][ks]), "+a"(vf[nt][ks]));
     __builtin_amdgcn_s_waitcnt(0);  // the next step's tiles have landed
     __syncthreads();                 // ... for every wave; this step's LDS is no longer read
-  }
+    c_ph = n_ph;
+    c_hh = n_hh;
+    c_k = n_k;
+    c_sub = n_sub;
+    advance(n_ph, n_hh, n_k, n_sub);
+  };
+  int t = 0;
+  for (; t < steps_full; ++t) step(t, false);
+  for (; t < n_steps; ++t) step(t, true);
 
   // write dK and dV of the block: through LDS as [key][d], then 16-byte rows
+  const float scale = p.softmax_scale;
   __bf16* tk = reinterpret_cast<__bf16*>(smem);                        // [BK][D + 8]
   __bf16* tv = reinterpret_cast<__bf16*>(smem) + BK * (D + 8);         // [BK][D + 8]
 #pragma unroll
@@ -262,7 +333,7 @@ __global__ void __launch_bounds__(256) bwd_main(cowa_params p, SchedView sv, con
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
         const int key = wave * C::NKW + nt * 16 + lr, d = md * 16 + 4 * lg + rr;
-        tk[key * (D + 8) + d] = (__bf16)dka[md][nt][rr];
+        tk[key * (D + 8) + d] = (__bf16)(scale * dka[md][nt][rr]);
         tv[key * (D + 8) + d] = (__bf16)dva[md][nt][rr];
       }
   __syncthreads();
@@ -283,19 +354,21 @@ hipError_t launch_main(const cowa_params& p, const SchedView& sv, const void* q,
                        const void* d_o, const float* lse, const float* dsum, void* dk, void* dv,
                        hipStream_t stream) {
   using C = BwdCfg<D, BK>;
-  static_assert(C::LDS_BYTES <= 160 * 1024, "LDS budget");
+  static_assert(C::OUT_BYTES <= C::LDS_MAX && C::MAIN_BYTES < C::LDS_MAX, "LDS budget");
+  if (sv.n_qt > C::max_qblocks()) return hipErrorInvalidValue;
   auto kern = bwd_main<D, BK>;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_MAX);
     if (err != hipSuccess) return err;
     attr_set = true;
   }
   const unsigned blocks = (unsigned)sv.n_kt * p.h_k * p.batch;
-  hipLaunchKernelGGL(kern, dim3(blocks), dim3(256), C::LDS_BYTES, stream, p, sv, static_cast<const __bf16*>(q),
-                     static_cast<const __bf16*>(k), static_cast<const __bf16*>(v), static_cast<const __bf16*>(d_o),
-                     lse, dsum, static_cast<__bf16*>(dk), static_cast<__bf16*>(dv));
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(256), C::lds_bytes(sv.n_qt), stream, p, sv,
+                     static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), static_cast<const __bf16*>(v),
+                     static_cast<const __bf16*>(d_o), lse, dsum, static_cast<__bf16*>(dk),
+                     static_cast<__bf16*>(dv));
   return hipGetLastError();
 }
 
@@ -329,7 +402,7 @@ __global__ void __launch_bounds__(512) bwd_dq_kernel(cowa_params p, SchedView sv
   const int hk = hgi / (G / hpw);
   const int h0 = hgi * hpw;
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int lr = lane & 15, lg = lane >> 4;
   const int h = h0 + wave / WAVES_PER_HEAD;
   const int64_t q_first = (int64_t)i * BQ + (wave % WAVES_PER_HEAD) * NQW;
@@ -341,8 +414,8 @@ __global__ void __launch_bounds__(512) bwd_dq_kernel(cowa_params p, SchedView sv
   const int e0 = sv.fwd_row_ptr[r], e1 = sv.fwd_row_ptr[r + 1];
   if (e0 < e1) {
     const int64_t kf = (int64_t)(sv.fwd_ent[e0] >> 1) * BK;
-    load_tile<D, BK>(kbase, kf, p.n_k, smem, wave, nw, lane);
-    load_tile<D, BK>(vbase, kf, p.n_k, smem + T::BYTES, wave, nw, lane);
+    load_tile_nw<D, BK>(kbase, (int)kf, p.n_k, smem, wave, nw, lane);
+    load_tile_nw<D, BK>(vbase, (int)kf, p.n_k, smem + T::BYTES, wave, nw, lane);
   }
 
   // Q^T and dO^T fragments (B operands): query column nt*16 + lr, d = ks*32 + 8*lg + 0..7;
@@ -386,8 +459,8 @@ __global__ void __launch_bounds__(512) bwd_dq_kernel(cowa_params p, SchedView sv
     if (e + 1 < e1) {
       const int64_t kf = (int64_t)(sv.fwd_ent[e + 1] >> 1) * BK;
       unsigned char* nb = smem + (buf ^ 1) * 2 * T::BYTES;
-      load_tile<D, BK>(kbase, kf, p.n_k, nb, wave, nw, lane);
-      load_tile<D, BK>(vbase, kf, p.n_k, nb + T::BYTES, wave, nw, lane);
+      load_tile_nw<D, BK>(kbase, (int)kf, p.n_k, nb, wave, nw, lane);
+      load_tile_nw<D, BK>(vbase, (int)kf, p.n_k, nb + T::BYTES, wave, nw, lane);
     }
     const unsigned char* Kt = smem + buf * 2 * T::BYTES;
     const unsigned char* Vt = Kt + T::BYTES;
@@ -497,6 +570,11 @@ hipError_t launch_dq(const cowa_params& p, const SchedView& sv, const void* q, c
 }
 
 }  // namespace
+
+int bwd_main_max_qblocks(int d, int tk) {
+  if (d == 128) return tk == 128 ? BwdCfg<128, 128>::max_qblocks() : BwdCfg<128, 64>::max_qblocks();
+  return tk == 128 ? BwdCfg<64, 128>::max_qblocks() : BwdCfg<64, 64>::max_qblocks();
+}
 
 bool bwd_bf16_supported(int d, int tq, int tk) {
   return (d == 64 || d == 128) && (tq == 64 || tq == 128) && (tk == 64 || tk == 128);

@@ -56,7 +56,7 @@ __global__ void __launch_bounds__(512) fwd_bf16_kernel(cowa_params p, SchedView 
   const int hk = hgi / (G / hpw);
   const int h0 = hgi * hpw;  // first QO head of this workgroup (all in KV group hk)
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int lr = lane & 15, lg = lane >> 4;
   const int h = h0 + wave / WAVES_PER_HEAD;
   const int64_t q_first = (int64_t)i * BQ + (wave % WAVES_PER_HEAD) * NQW;
@@ -70,8 +70,8 @@ __global__ void __launch_bounds__(512) fwd_bf16_kernel(cowa_params p, SchedView 
   // buffer s: K at smem + 2 s BYTES, V right after it
   if (e0 < e1) {
     const int64_t kf = (int64_t)(sv.fwd_ent[e0] >> 1) * BK;
-    load_tile<D, BK>(kbase, kf, p.n_k, smem, wave, nw, lane);
-    load_tile<D, BK>(vbase, kf, p.n_k, smem + T::BYTES, wave, nw, lane);
+    load_tile_nw<D, BK>(kbase, (int)kf, p.n_k, smem, wave, nw, lane);
+    load_tile_nw<D, BK>(vbase, (int)kf, p.n_k, smem + T::BYTES, wave, nw, lane);
   }
 
   // Q^T fragments (B operand): query column nt*16 + lr, d = ks*32 + 8*lg + 0..7
@@ -110,8 +110,8 @@ __global__ void __launch_bounds__(512) fwd_bf16_kernel(cowa_params p, SchedView 
     if (e + 1 < e1) {  // prefetch the next block into the other buffer
       const int64_t kf = (int64_t)(sv.fwd_ent[e + 1] >> 1) * BK;
       unsigned char* nb = smem + (buf ^ 1) * 2 * T::BYTES;
-      load_tile<D, BK>(kbase, kf, p.n_k, nb, wave, nw, lane);
-      load_tile<D, BK>(vbase, kf, p.n_k, nb + T::BYTES, wave, nw, lane);
+      load_tile_nw<D, BK>(kbase, (int)kf, p.n_k, nb, wave, nw, lane);
+      load_tile_nw<D, BK>(vbase, (int)kf, p.n_k, nb + T::BYTES, wave, nw, lane);
     }
     const unsigned char* Kt = smem + buf * 2 * T::BYTES;
     const unsigned char* Vt = Kt + T::BYTES;

@@ -1,8 +1,9 @@
 // Shared building blocks of the matrix-core kernels (gfx950).
 //
-// * bf16 row-major tiles in LDS with 16-byte chunks XOR-swizzled by row, so
-//   that 16 lanes reading the same chunk of 16 consecutive rows, or the
-//   transposing reads below, touch distinct banks;
+// * bf16 row-major tiles in LDS with 16-byte chunks XOR-swizzled by row (see
+//   swz below), so that both read patterns of the kernels touch distinct
+//   banks: 16 lanes reading the same chunk of 16 consecutive rows
+//   (ds_read_b128), and the transposing reads below;
 // * direct global -> LDS copies of such tiles (global_load_lds, 16 bytes per
 //   lane: lane l of one instruction lands at LDS base + 16 l);
 // * transposing LDS reads (ds_read_b64_tr_b16).  Within each group of 16
@@ -40,33 +41,84 @@ __device__ inline int xcd_remap(int id, int total) {
   return chunk * 8 + (slot & 7);
 }
 
+// XOR applied to the 16-byte chunk index of a row; depends on row % 16 only.
+// A read of 16 lanes covers 256 bytes; the choice below keeps every such read
+// of the two patterns on distinct four-byte banks whether the LDS serves 128
+// or 256 bytes per clock (checked exhaustively over the bank arithmetic):
+//  * ds_read_b128 of one chunk in rows r .. r+15 (r a multiple of 16): the
+//    map row -> swz is one-to-one on 16 rows, and on any 8 consecutive rows
+//    it is one-to-one modulo 8;
+//  * ds_read_b64_tr_b16 of rows r .. r+3, chunks c, c+1 (c even) per 16 lanes:
+//    swz / 2 differs between the 4 rows (and between 8 rows for 32 lanes), so
+//    c ^ swz and (c+1) ^ swz never meet.
+template <int CH>
+__device__ inline int swz(int row) {
+  static_assert(CH == 8 || CH == 16, "head_dim 64 or 128");
+  if constexpr (CH == 16) return ((row & 7) << 1) | (((row >> 2) ^ (row >> 3)) & 1);
+  return ((row >> 1) & 1) | (((row ^ (row >> 2)) & 1) << 1) | (((row ^ (row >> 1) ^ (row >> 3)) & 1) << 2);
+}
+
 // A swizzled tile of ROWS rows x D bf16 columns (row pitch 2 D bytes).
 template <int D, int ROWS>
 struct SwzTile {
   static constexpr int CH = D / 8;             // 16-byte chunks per row
   static constexpr int BYTES = ROWS * D * 2;
   static constexpr int LOADS = BYTES / 1024;   // 1 KB direct loads per tile
-  __device__ static inline int off(int row, int chunk) { return row * (D * 2) + ((chunk ^ (row % CH)) << 4); }
+  __device__ static inline int off(int row, int chunk) { return row * (D * 2) + ((chunk ^ swz<CH>(row)) << 4); }
   // byte address of the 8-byte group holding column col (a multiple of 4)
   __device__ static inline int off_col(int row, int col) { return off(row, col >> 3) + ((col & 7) << 1); }
 };
 
 // Copy rows [first, first + ROWS) of a row-major [n_rows][D] bf16 matrix into
 // a swizzled LDS tile; rows past n_rows repeat row n_rows - 1 (callers mask
-// them).  Every wave of the workgroup takes every nw-th 1 KB piece.
+// them).  The NW waves of the workgroup take the 1 KB pieces in turn; wave must
+// be wave-uniform.  Since NW pieces span a multiple of 16 rows, a lane's row
+// modulo 16, and so its swizzled chunk, is the same in every piece it copies.
+template <int D, int ROWS, int NW>
+__device__ inline void load_tile(const __bf16* base, int first, int n_rows, unsigned char* lds, int wave, int lane) {
+  using T = SwzTile<D, ROWS>;
+  constexpr int RPL = 1024 / (D * 2);  // rows per piece
+  static_assert(T::LOADS % NW == 0 && (NW * RPL) % 16 == 0, "piece layout");
+  const int row0 = wave * RPL + lane / T::CH;
+  const int col = (((lane % T::CH) ^ swz<T::CH>(row0)) << 3);
+#pragma unroll
+  for (int n = 0; n < T::LOADS / NW; ++n) {
+    int r = first + n * NW * RPL + row0;
+    r = r < n_rows ? r : n_rows - 1;
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(base + (int64_t)r * D + col),
+                                     (lds_void*)(lds + (n * NW + wave) * 1024), 16, 0, 0);
+  }
+}
+
+// The same for any wave count (a lane's chunk recomputed per piece).
 template <int D, int ROWS>
-__device__ inline void load_tile(const __bf16* base, int64_t first, int64_t n_rows, unsigned char* lds, int wave,
-                                 int nw, int lane) {
+__device__ inline void load_tile_any(const __bf16* base, int first, int n_rows, unsigned char* lds, int wave, int nw,
+                                     int lane) {
   using T = SwzTile<D, ROWS>;
   for (int n = wave; n < T::LOADS; n += nw) {
     const int flat = n * 64 + lane;  // 16-byte unit index == LDS position
     const int row = flat / T::CH, slot = flat % T::CH;
-    const int chunk = slot ^ (row % T::CH);
-    int64_t r = first + row;
-    if (r >= n_rows) r = n_rows - 1;
-    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(base + r * D + chunk * 8),
+    const int chunk = slot ^ swz<T::CH>(row);
+    int r = first + row;
+    r = r < n_rows ? r : n_rows - 1;
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(base + (int64_t)r * D + chunk * 8),
                                      (lds_void*)(lds + n * 1024), 16, 0, 0);
   }
+}
+
+// Dispatch on a wave-uniform wave count.
+template <int D, int ROWS>
+__device__ inline void load_tile_nw(const __bf16* base, int first, int n_rows, unsigned char* lds, int wave, int nw,
+                                    int lane) {
+  using T = SwzTile<D, ROWS>;
+  constexpr int RPL = 1024 / (D * 2);
+  if constexpr (T::LOADS % 8 == 0 && (8 * RPL) % 16 == 0) {
+    if (nw == 8) return load_tile<D, ROWS, 8>(base, first, n_rows, lds, wave, lane);
+  }
+  if constexpr (T::LOADS % 4 == 0 && (4 * RPL) % 16 == 0) {
+    if (nw == 4) return load_tile<D, ROWS, 4>(base, first, n_rows, lds, wave, lane);
+  }
+  load_tile_any<D, ROWS>(base, first, n_rows, lds, wave, nw, lane);
 }
 
 // 16-byte row fragment: row `row`, columns 8 chunk .. 8 chunk + 7.
@@ -95,6 +147,30 @@ __device__ inline bf16x8 read_tr8_plain(const unsigned char* tile, int pitch, in
   const int col = c0 + 4 * (lr & 3);
   const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(tile + row * pitch + col * 2));
   const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(tile + (row + 16) * pitch + col * 2));
+  const bf16x4 a = __builtin_bit_cast(bf16x4, lo), b = __builtin_bit_cast(bf16x4, hi);
+  return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+}
+
+// Per-lane byte offsets of the two read patterns, for rows 0..15 of a tile;
+// since the swizzle depends on row % 16, rows 16 m + ... add 16 m D 2 bytes
+// (a constant the compiler folds into the instruction's offset field).
+//  row fragment: lane (lr, lg) reads row lr, chunk 4 ks + lg;
+template <int D>
+__device__ inline int row8_off(int lr, int lg, int ks) {
+  return lr * (D * 2) + (((4 * ks + lg) ^ swz<D / 8>(lr)) << 4);
+}
+//  transposing read: lane (lr, lg) points at row 4 lg + lr / 4, column 16 md + 4 (lr % 4).
+template <int D>
+__device__ inline int tr8_off(int lr, int lg, int md) {
+  const int row = 4 * lg + (lr >> 2), col = 16 * md + 4 * (lr & 3);
+  return row * (D * 2) + (((col >> 3) ^ swz<D / 8>(row)) << 4) + ((col & 7) << 1);
+}
+__device__ inline bf16x8 ld_row8(const unsigned char* p) { return *reinterpret_cast<const bf16x8*>(p); }
+// the transposed operand of rows r0 .. r0+31 (p at row r0 of the pattern above;
+// row_bytes = 2 D): rows r0 + 4 g + t in slots 0..3, rows r0 + 16 + 4 g + t in 4..7
+__device__ inline bf16x8 ld_tr8(const unsigned char* p, int row_bytes) {
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 16 * row_bytes));
   const bf16x4 a = __builtin_bit_cast(bf16x4, lo), b = __builtin_bit_cast(bf16x4, hi);
   return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
 }

@@ -74,7 +74,8 @@ __host__ __device__ inline Geo32 geo32(const HeadGeo& g) {
 // Same predicate as legal_pair for in-range positions (q < n_q, k < n_k).
 __host__ __device__ inline bool legal32(const Geo32& g, int32_t q, int32_t k) {
   const int32_t d = q + g.off - k;
-  return q < g.n_q && k < g.n_k && d >= 0 && (d < g.w_near || k < g.w_sink || (d >= g.lo && d < g.hi));
+  // bitwise, not short-circuit: a mask evaluated without branches
+  return (q < g.n_q) & (k < g.n_k) & (d >= 0) & ((d < g.w_near) | (k < g.w_sink) | ((d >= g.lo) & (d < g.hi)));
 }
 
 // Up to three inclusive ranges, merged (overlapping or adjacent ranges join).
