@@ -65,11 +65,14 @@ struct BwdCfg {
   static constexpr int MD = D / 16;       // d tiles
   static constexpr int KSQ = BQ / 32;     // k-steps over queries
   using QT = SwzTile<D, BQ>;              // Q or dO rows of one step
-  static constexpr int ROWV = 2 * BQ * 4; // per-step row values: base-2 LSE [BQ], then D [BQ]
-  // LDS: Q of stages 0, 1; dO of stages 0, 1; row values of stages 0, 1
-  static constexpr int Q_OFF0 = 0, Q_OFF1 = QT::BYTES, DO_OFF0 = 2 * QT::BYTES, DO_OFF1 = 3 * QT::BYTES;
-  static constexpr int RV_OFF0 = 4 * QT::BYTES, RV_OFF1 = 4 * QT::BYTES + ROWV;
-  static constexpr int MAIN_BYTES = 4 * QT::BYTES + 2 * ROWV;  // then the column's entry lists
+  static constexpr int ROWV = 2 * BQ * 4; // per-step row values: LSE [BQ], then D [BQ]
+  // LDS: a ring of three stages (Q, dO, row values), then the column's entry lists
+  static constexpr int NST = 3;
+  __device__ static int q_off(int s) { return s * QT::BYTES; }
+  __device__ static int do_off(int s) { return (NST + s) * QT::BYTES; }
+  __device__ static int rv_off(int s) { return 2 * NST * QT::BYTES + s * ROWV; }
+  static constexpr int MAIN_BYTES = 2 * NST * QT::BYTES + NST * ROWV;
+  static constexpr int LOADS_PER_STEP = 2 * QT::LOADS / 4 + 1;  // direct loads each wave issues per step
   static constexpr int OUT_BYTES = 2 * BK * (D + 8) * 2;        // dK, dV staging at the end
   static constexpr int LDS_MAX = 160 * 1024;
   // LDS for a schedule with n_qt query blocks
@@ -135,7 +138,8 @@ __global__ void __launch_bounds__(256) bwd_main(cowa_params p, SchedView sv, con
   const int steps_full = G * n_full * subs, n_steps = G * n_ent * subs;
   // cursor (phase: 0 full / 1 partial, QO head, list index, sub-block)
   int c_ph = n_full > 0 ? 0 : 1, c_hh = 0, c_k = 0, c_sub = 0;  // step being computed
-  int n_ph = c_ph, n_hh = 0, n_k = 0, n_sub = 0;               // step being staged
+  int n1_ph = c_ph, n1_hh = 0, n1_k = 0, n1_sub = 0;            // the next step (staged)
+  int n2_ph = c_ph, n2_hh = 0, n2_k = 0, n2_sub = 0;            // the step after (being staged)
   auto advance = [&](int& ph, int& hh, int& kk, int& sub) {
     if (++sub == subs) {
       sub = 0;
@@ -155,35 +159,34 @@ __global__ void __launch_bounds__(256) bwd_main(cowa_params p, SchedView sv, con
     return __builtin_amdgcn_readfirstlane(list[idx]);
   };
 
-  // Q and dO rows of a step go global -> LDS directly; its LSE (as base 2; a
-  // row without keys or past n_q gets +inf, so P = 0) and D values go through
-  // registers (every wave loads and stores the same 64 values, which keeps
-  // the step free of branches).  A cursor past the last step stages a copy of
-  // the last head's rows, never read.
-  float st_l2 = 0.f, st_dd = 0.f;
-  auto stage = [&](uint32_t ent, int hh, int sub, int q_off, int do_off) {
+  // Every operand of a step goes global -> LDS directly, through copies the
+  // compiler does not track (dma16/dma4): the Q and dO tiles, and the LSE and
+  // D values of its 64 rows (waves 0 and 2 copy the LSE, 1 and 3 the D values,
+  // the same data twice).  Each wave issues LOADS_PER_STEP copies per step and
+  // waits for them two steps later.  Rows past n_q repeat row n_q - 1; they
+  // occur in partial blocks only, where the mask gives them P = 0.  A cursor
+  // past the last step stages a copy of the last head's rows, never read.
+  const uint32_t smem_base = lds_addr(smem);
+  auto stage = [&](uint32_t ent, int hh, int sub, int slot) {
     hh = hh < G ? hh : G - 1;
     const int q0 = (int)(ent >> 1) * p.tile_q + sub * C::BQ;
     const int64_t row_base = ((int64_t)b * p.h_q + hk * G + hh) * p.n_q;
-    load_tile<D, C::BQ, 4>(q + row_base * D, q0, p.n_q, smem + q_off, wave, lane);
-    load_tile<D, C::BQ, 4>(d_o + row_base * D, q0, p.n_q, smem + do_off, wave, lane);
+    load_tile_asm<D, C::BQ, 4>(q + row_base * D, q0, p.n_q, smem_base + C::q_off(slot), wave, lane);
+    load_tile_asm<D, C::BQ, 4>(d_o + row_base * D, q0, p.n_q, smem_base + C::do_off(slot), wave, lane);
     const int r = q0 + lane;
     const int rc = r < p.n_q ? r : p.n_q - 1;
-    const float lv = lse[row_base + rc], dv0 = dsum[row_base + rc];
-    st_l2 = (r < p.n_q && lv != -INFINITY) ? lv * kLog2e : INFINITY;
-    st_dd = r < p.n_q ? dv0 : 0.f;
-  };
-  auto store_rowv = [&](int rv_off) {
-    float* rv = reinterpret_cast<float*>(smem + rv_off);
-    rv[lane] = st_l2;
-    rv[C::BQ + lane] = st_dd;
+    dma4(((wave & 1) ? dsum : lse) + row_base + rc,
+         __builtin_amdgcn_readfirstlane(smem_base + C::rv_off(slot) + (wave & 1) * C::BQ * 4));
   };
 
   __syncthreads();  // the entry lists are in LDS
+  // prologue: steps 0 and 1 in flight
   if (n_steps > 0) {
-    stage(entry_of(n_ph, n_k), n_hh, n_sub, C::Q_OFF0, C::DO_OFF0);
-    store_rowv(C::RV_OFF0);
-    advance(n_ph, n_hh, n_k, n_sub);
+    stage(entry_of(n2_ph, n2_k), n2_hh, n2_sub, 0);  // step 0
+    advance(n2_ph, n2_hh, n2_k, n2_sub);
+    n1_ph = n2_ph, n1_hh = n2_hh, n1_k = n2_k, n1_sub = n2_sub;
+    stage(entry_of(n2_ph, n2_k), n2_hh, n2_sub, 1);  // step 1
+    advance(n2_ph, n2_hh, n2_k, n2_sub);
   }
 
   // K and V rows of this wave's keys as B fragments: key nt*16 + lr, d = ks*32 + 8*lg + 0..7
@@ -217,86 +220,126 @@ __global__ void __launch_bounds__(256) bwd_main(cowa_params p, SchedView sv, con
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
-  // One step on stage st (0 or 1):
+  // One step on ring slot `slot`:
   //   S = Q K^T, dP = dO V^T, P = exp(S - LSE), dS = P (dP - D),
   //   dV^T += dO^T P, dK^T += Q^T dS (the softmax scale is applied to dK at the end).
   // The 64 rows are taken in two halves of 32 (one k-step of the dV/dK
-  // products), and the phases are ordered so that the matrix cores always have
-  // independent work while the vector units run a softmax:
-  //   S/dP(0) | S/dP(1) + softmax(0) | dV/dK(0) + softmax(1) | dV/dK(1).
-  // Scheduling fences keep the phases apart (and the live registers bounded).
+  // products).  The step is a fixed schedule of groups of four MFMAs, each
+  // with the LDS reads of the next group and, where there is one, a chunk of a
+  // softmax, so that the matrix cores always have independent work while the
+  // vector units run the exponentials:
+  //   S/dP(half 0) | S/dP(half 1) + softmax(half 0) | dV/dK(half 0) + softmax(half 1) | dV/dK(half 1)
+  // Scheduling fences between groups keep that order.
   f32x4 sacc[C::MTQ][C::NTK], pacc[C::MTQ][C::NTK];  // rows q = mt*16 + 4*lg + r, column key = nt*16 + lr
   bf16x8 pb[C::KSQ][C::NTK], sb[C::KSQ][C::NTK];     // P and dS as B operands, k-slots = queries of a half
-  auto sdp_half = [&](const unsigned char* qs, const unsigned char* dos, int hf) {
-#pragma unroll
-    for (int ks = 0; ks < C::KSD; ++ks)
-#pragma unroll
-      for (int mt = 2 * hf; mt < 2 * hf + 2; ++mt) {
-        const bf16x8 aq = ld_row8(qs + offr[ks] + mt * 16 * D * 2);
-        const bf16x8 ag = ld_row8(dos + offr[ks] + mt * 16 * D * 2);
-#pragma unroll
-        for (int nt = 0; nt < C::NTK; ++nt) {
-          sacc[mt][nt] = mfma16(aq, kf[nt][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sacc[mt][nt]);
-          pacc[mt][nt] = mfma16(ag, vf[nt][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : pacc[mt][nt]);
-        }
-      }
+  constexpr int NG = 2 * C::KSD;  // S/dP groups per half: (k-step, query tile)
+  static_assert(C::MTQ == 4 && C::MD == NG && (8 * C::NTK) % NG == 0, "group schedule layout");
+  // S/dP group gi of half hf: k-step gi / 2, query tile 2 hf + gi % 2
+  auto sdp_load = [&](const unsigned char* qs, const unsigned char* dos, int hf, int gi, bf16x8& fa, bf16x8& fb) {
+    const int ks = gi >> 1, mt = 2 * hf + (gi & 1);
+    fa = ld_row8(qs + offr[ks] + mt * 16 * D * 2);
+    fb = ld_row8(dos + offr[ks] + mt * 16 * D * 2);
   };
-  // P and dS of a half, rounded to bf16 in the B-operand layout: k-slot 4 i + t
-  // is query row (2 hf + i) * 16 + 4 lg + t.  In a partial block the masked
-  // pairs get P = 0 through an additive -inf in the exponent (an update that
-  // reads the MFMA result).
-  auto softmax_half = [&](const float* rowv, int hf, bool masked, int q0) {
-    const int qi0 = q0 + 4 * lg;
+  auto sdp_mfma = [&](int hf, int gi, const bf16x8& fa, const bf16x8& fb) {
+    const int ks = gi >> 1, mt = 2 * hf + (gi & 1);
+#pragma unroll
+    for (int nt = 0; nt < C::NTK; ++nt) {
+      sacc[mt][nt] = mfma16(fa, kf[nt][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sacc[mt][nt]);
+      pacc[mt][nt] = mfma16(fb, vf[nt][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : pacc[mt][nt]);
+    }
+  };
+  // dV/dK group md of half hf: d tile md, queries of the half as k-slots
+  auto dvdk_load = [&](const unsigned char* qs, const unsigned char* dos, int hf, int md, bf16x8& fa, bf16x8& fb) {
+    fa = ld_tr8(dos + offt[md] + hf * 32 * D * 2, D * 2);
+    fb = ld_tr8(qs + offt[md] + hf * 32 * D * 2, D * 2);
+  };
+  auto dvdk_mfma = [&](int hf, int md, const bf16x8& fa, const bf16x8& fb) {
+#pragma unroll
+    for (int nt = 0; nt < C::NTK; ++nt) {
+      dva[md][nt] = mfma16(fa, pb[hf][nt], dva[md][nt]);
+      dka[md][nt] = mfma16(fb, sb[hf][nt], dka[md][nt]);
+    }
+  };
+  // Softmax chunk ci of half hf: elements e = ci * EPC .. ci * EPC + EPC - 1 of
+  // the lane's 8 NTK, where element e is row r = e % 4 of the lane's four in
+  // query tile 2 hf + e / (4 NTK), key tile (e / 4) % NTK.  P and dS are rounded
+  // to bf16 into the B-operand layout: k-slot 4 i + r is query row
+  // (2 hf + i) * 16 + 4 lg + r.  In a partial block the masked pairs get P = 0
+  // through a -inf exponent, selected after the exponent has read the MFMA result.
+  constexpr int EPC = 8 * C::NTK / NG;
+  auto soft_chunk = [&](int hf, int ci, const float4 (&l4)[2], const float4 (&d4)[2], bool masked, int q0) {
+#pragma unroll
+    for (int jj = 0; jj < EPC; ++jj) {
+      const int e = ci * EPC + jj, r = e & 3, nt = (e >> 2) % C::NTK, i = e / (4 * C::NTK), mt = 2 * hf + i;
+      const float lv = r == 0 ? l4[i].x : r == 1 ? l4[i].y : r == 2 ? l4[i].z : l4[i].w;
+      const float dd = r == 0 ? d4[i].x : r == 1 ? d4[i].y : r == 2 ? d4[i].z : d4[i].w;
+      float x = fmaf(sacc[mt][nt][r], c, -lv * kLog2e);
+      // (a row of a full block has a finite LSE; a masked pair may have LSE = -inf)
+      if (masked) x = legal32(g, q0 + 4 * lg + mt * 16 + r, k0 + nt * 16) ? x : -INFINITY;
+      const float pv = __builtin_amdgcn_exp2f(x);
+      pb[hf][nt][4 * i + r] = (__bf16)pv;
+      sb[hf][nt][4 * i + r] = (__bf16)(pv * (pacc[mt][nt][r] - dd));
+    }
+  };
+  auto load_rowv = [&](const float* rowv, int hf, float4 (&l4)[2], float4 (&d4)[2]) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int mt = 2 * hf + i;
-      const float4 l4 = *reinterpret_cast<const float4*>(rowv + mt * 16 + 4 * lg);
-      const float4 d4 = *reinterpret_cast<const float4*>(rowv + C::BQ + mt * 16 + 4 * lg);
-      const float l2[4] = {l4.x, l4.y, l4.z, l4.w}, dd[4] = {d4.x, d4.y, d4.z, d4.w};
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr)
-#pragma unroll
-        for (int nt = 0; nt < C::NTK; ++nt) {
-          float x = fmaf(sacc[mt][nt][rr], c, -l2[rr]);
-          if (masked) x += legal32(g, qi0 + mt * 16 + rr, k0 + nt * 16) ? 0.f : -INFINITY;
-          const float pv = __builtin_amdgcn_exp2f(x);
-          pb[hf][nt][4 * i + rr] = (__bf16)pv;
-          sb[hf][nt][4 * i + rr] = (__bf16)(pv * (pacc[mt][nt][rr] - dd[rr]));
-        }
-    }
-  };
-  auto dvdk_half = [&](const unsigned char* qs, const unsigned char* dos, int hf) {
-#pragma unroll
-    for (int md = 0; md < C::MD; ++md) {
-      const bf16x8 ag = ld_tr8(dos + offt[md] + hf * 32 * D * 2, D * 2);
-      const bf16x8 aq = ld_tr8(qs + offt[md] + hf * 32 * D * 2, D * 2);
-#pragma unroll
-      for (int nt = 0; nt < C::NTK; ++nt) {
-        dva[md][nt] = mfma16(ag, pb[hf][nt], dva[md][nt]);
-        dka[md][nt] = mfma16(aq, sb[hf][nt], dka[md][nt]);
-      }
+      l4[i] = *reinterpret_cast<const float4*>(rowv + (2 * hf + i) * 16 + 4 * lg);
+      d4[i] = *reinterpret_cast<const float4*>(rowv + C::BQ + (2 * hf + i) * 16 + 4 * lg);
     }
   };
 
-  auto step = [&](int t, bool masked) {
-    const int st = t & 1;
-    const unsigned char* qs = smem + (st ? C::Q_OFF1 : C::Q_OFF0);
-    const unsigned char* dos = smem + (st ? C::DO_OFF1 : C::DO_OFF0);
-    const float* rowv = reinterpret_cast<const float*>(smem + (st ? C::RV_OFF1 : C::RV_OFF0));
+  int slot = 0;  // ring slot of the step being computed (t mod 3)
+  auto step = [&](bool masked) {
+    const int slot2 = slot == 0 ? 2 : slot - 1;  // (t + 2) mod 3
+    const unsigned char* qs = smem + C::q_off(slot);
+    const unsigned char* dos = smem + C::do_off(slot);
+    const float* rowv = reinterpret_cast<const float*>(smem + C::rv_off(slot));
     const int q0 = (int)(entry_of(c_ph, c_k) >> 1) * p.tile_q + c_sub * C::BQ;
-    stage(entry_of(n_ph, n_k), n_hh, n_sub, st ? C::Q_OFF0 : C::Q_OFF1, st ? C::DO_OFF0 : C::DO_OFF1);
+    stage(entry_of(n2_ph, n2_k), n2_hh, n2_sub, slot2);
 
-    sdp_half(qs, dos, 0);
+    bf16x8 fa[2], fb[2];  // operand fragments, one group ahead
+    float4 l4[2], d4[2];  // LSE and D of the half in the softmax
+    sdp_load(qs, dos, 0, 0, fa[0], fb[0]);
     __builtin_amdgcn_sched_barrier(0);
-    sdp_half(qs, dos, 1);
-    softmax_half(rowv, 0, masked, q0);
-    __builtin_amdgcn_sched_barrier(0);
-    dvdk_half(qs, dos, 0);
-    softmax_half(rowv, 1, masked, q0);
-    __builtin_amdgcn_sched_barrier(0);
-    dvdk_half(qs, dos, 1);
+#pragma unroll
+    for (int gi = 0; gi < NG; ++gi) {  // S/dP of half 0
+      if (gi + 1 < NG)
+        sdp_load(qs, dos, 0, gi + 1, fa[(gi + 1) & 1], fb[(gi + 1) & 1]);
+      else
+        sdp_load(qs, dos, 1, 0, fa[(gi + 1) & 1], fb[(gi + 1) & 1]);
+      if (gi == NG - 1) load_rowv(rowv, 0, l4, d4);
+      sdp_mfma(0, gi, fa[gi & 1], fb[gi & 1]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int gi = 0; gi < NG; ++gi) {  // S/dP of half 1, softmax of half 0
+      if (gi + 1 < NG)
+        sdp_load(qs, dos, 1, gi + 1, fa[(gi + 1) & 1], fb[(gi + 1) & 1]);
+      else
+        dvdk_load(qs, dos, 0, 0, fa[(gi + 1) & 1], fb[(gi + 1) & 1]);
+      sdp_mfma(1, gi, fa[gi & 1], fb[gi & 1]);
+      soft_chunk(0, gi, l4, d4, masked, q0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    load_rowv(rowv, 1, l4, d4);
+#pragma unroll
+    for (int md = 0; md < C::MD; ++md) {  // dV/dK of half 0, softmax of half 1
+      if (md + 1 < C::MD)
+        dvdk_load(qs, dos, 0, md + 1, fa[(md + 1) & 1], fb[(md + 1) & 1]);
+      else
+        dvdk_load(qs, dos, 1, 0, fa[(md + 1) & 1], fb[(md + 1) & 1]);
+      dvdk_mfma(0, md, fa[md & 1], fb[md & 1]);
+      soft_chunk(1, md, l4, d4, masked, q0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int md = 0; md < C::MD; ++md) {  // dV/dK of half 1
+      if (md + 1 < C::MD) dvdk_load(qs, dos, 1, md + 1, fa[(md + 1) & 1], fb[(md + 1) & 1]);
+      dvdk_mfma(1, md, fa[md & 1], fb[md & 1]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
 
-    store_rowv(st ? C::RV_OFF0 : C::RV_OFF1);
     // Register placement (the library builds this file with MFMA results in
     // VGPRs): the dK/dV accumulators stay in VGPRs and the K/V fragments in
     // AGPRs, which the MFMAs read directly as B operands.  These empty
@@ -310,18 +353,22 @@ __global__ void __launch_bounds__(256) bwd_main(cowa_params p, SchedView sv, con
     for (int nt = 0; nt < C::NTK; ++nt)
 #pragma unroll
       for (int ks = 0; ks < C::KSD; ++ks) asm volatile("" : "+a"(kf[nt][ks]), "+a"(vf[nt][ks]));
-    __builtin_amdgcn_s_waitcnt(0);  // the next step's tiles have landed
-    __syncthreads();                 // ... for every wave; this step's LDS is no longer read
-    c_ph = n_ph;
-    c_hh = n_hh;
-    c_k = n_k;
-    c_sub = n_sub;
-    advance(n_ph, n_hh, n_k, n_sub);
+    // the next step's operands have landed (only the step after may still be in
+    // flight), for every wave; and this step's slot is no longer read
+    __builtin_amdgcn_s_waitcnt(vmcnt_only(C::LOADS_PER_STEP));
+    __syncthreads();
+    c_ph = n1_ph, c_hh = n1_hh, c_k = n1_k, c_sub = n1_sub;
+    n1_ph = n2_ph, n1_hh = n2_hh, n1_k = n2_k, n1_sub = n2_sub;
+    advance(n2_ph, n2_hh, n2_k, n2_sub);
+    slot = slot == 2 ? 0 : slot + 1;
   };
   int t = 0;
-  for (; t < steps_full; ++t) step(t, false);
-  for (; t < n_steps; ++t) step(t, true);
+  for (; t < steps_full; ++t) step(false);
+  for (; t < n_steps; ++t) step(true);
 
+  // the copies staged past the last step must land before their LDS is reused
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
   // write dK and dV of the block: through LDS as [key][d], then 16-byte rows
   const float scale = p.softmax_scale;
   __bf16* tk = reinterpret_cast<__bf16*>(smem);                        // [BK][D + 8]

@@ -90,6 +90,44 @@ __device__ inline void load_tile(const __bf16* base, int first, int n_rows, unsi
   }
 }
 
+// Global -> LDS copies issued as inline assembly: 16 (dma16) or 4 (dma4) bytes
+// per lane, lane l landing at LDS byte address lds_base + 16 l (or 4 l).  The
+// compiler does not see these as memory operations, so it neither counts them
+// in its own s_waitcnt arithmetic nor makes unrelated LDS reads wait for them;
+// the caller waits for them explicitly (s_waitcnt vmcnt) before their data is
+// read and before the LDS they target is reused.  lds_base must be uniform.
+__device__ inline uint32_t lds_addr(const unsigned char* p) {
+  return (uint32_t)(uintptr_t)(lds_void*)p;
+}
+__device__ inline void dma16(const void* gptr, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(gptr), "s"(lds_base)
+               : "memory", "m0");
+}
+__device__ inline void dma4(const void* gptr, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+               :
+               : "v"(gptr), "s"(lds_base)
+               : "memory", "m0");
+}
+
+// load_tile through dma16 (same layout and piece order).
+template <int D, int ROWS, int NW>
+__device__ inline void load_tile_asm(const __bf16* base, int first, int n_rows, uint32_t lds, int wave, int lane) {
+  using T = SwzTile<D, ROWS>;
+  constexpr int RPL = 1024 / (D * 2);
+  static_assert(T::LOADS % NW == 0 && (NW * RPL) % 16 == 0, "piece layout");
+  const int row0 = wave * RPL + lane / T::CH;
+  const int col = (((lane % T::CH) ^ swz<T::CH>(row0)) << 3);
+#pragma unroll
+  for (int n = 0; n < T::LOADS / NW; ++n) {
+    int r = first + n * NW * RPL + row0;
+    r = r < n_rows ? r : n_rows - 1;
+    dma16(base + (int64_t)r * D + col, __builtin_amdgcn_readfirstlane(lds + (n * NW + wave) * 1024));
+  }
+}
+
 // The same for any wave count (a lane's chunk recomputed per piece).
 template <int D, int ROWS>
 __device__ inline void load_tile_any(const __bf16* base, int first, int n_rows, unsigned char* lds, int wave, int nw,
