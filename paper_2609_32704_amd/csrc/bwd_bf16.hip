@@ -55,10 +55,11 @@ __global__ void __launch_bounds__(256) bwd_pre(const __bf16* __restrict__ o, con
   if (row < rows && ch == 0) dsum[row] = part;
 }
 
-template <int D, int BK>
+template <int D, int BK, int NW_ = 4>
 struct BwdCfg {
+  static constexpr int NW = NW_;          // waves per workgroup
   static constexpr int BQ = 64;           // query rows per step
-  static constexpr int NKW = BK / 4;      // keys per wave
+  static constexpr int NKW = BK / NW;     // keys per wave
   static constexpr int NTK = NKW / 16;    // key tiles per wave
   static constexpr int MTQ = BQ / 16;     // query tiles per step
   static constexpr int KSD = D / 32;      // k-steps over d
@@ -72,7 +73,7 @@ struct BwdCfg {
   __device__ static int do_off(int s) { return (NST + s) * QT::BYTES; }
   __device__ static int rv_off(int s) { return 2 * NST * QT::BYTES + s * ROWV; }
   static constexpr int MAIN_BYTES = 2 * NST * QT::BYTES + NST * ROWV;
-  static constexpr int LOADS_PER_STEP = 2 * QT::LOADS / 4 + 1;  // direct loads each wave issues per step
+  static constexpr int LOADS_PER_STEP = 2 * QT::LOADS / NW + 1;  // direct loads each wave issues per step
   static constexpr int OUT_BYTES = 2 * BK * (D + 8) * 2;        // dK, dV staging at the end
   static constexpr int LDS_MAX = 160 * 1024;
   // LDS for a schedule with n_qt query blocks
@@ -83,13 +84,13 @@ struct BwdCfg {
   static int max_qblocks() { return (LDS_MAX - MAIN_BYTES) / 4; }
 };
 
-template <int D, int BK>
-__global__ void __launch_bounds__(256) bwd_main(cowa_params p, SchedView sv, const __bf16* __restrict__ q,
+template <int D, int BK, int NW>
+__global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv, const __bf16* __restrict__ q,
                                                 const __bf16* __restrict__ k, const __bf16* __restrict__ v,
                                                 const __bf16* __restrict__ d_o, const float* __restrict__ lse,
                                                 const float* __restrict__ dsum, __bf16* __restrict__ dk,
                                                 __bf16* __restrict__ dv) {
-  using C = BwdCfg<D, BK>;
+  using C = BwdCfg<D, BK, NW>;
   extern __shared__ __align__(1024) unsigned char smem[];
 
   const int total = sv.n_kt * p.h_k * p.batch;
@@ -171,8 +172,8 @@ __global__ void __launch_bounds__(256) bwd_main(cowa_params p, SchedView sv, con
     hh = hh < G ? hh : G - 1;
     const int q0 = (int)(ent >> 1) * p.tile_q + sub * C::BQ;
     const int64_t row_base = ((int64_t)b * p.h_q + hk * G + hh) * p.n_q;
-    load_tile_asm<D, C::BQ, 4>(q + row_base * D, q0, p.n_q, smem_base + C::q_off(slot), wave, lane);
-    load_tile_asm<D, C::BQ, 4>(d_o + row_base * D, q0, p.n_q, smem_base + C::do_off(slot), wave, lane);
+    load_tile_asm<D, C::BQ, NW>(q + row_base * D, q0, p.n_q, smem_base + C::q_off(slot), wave, lane);
+    load_tile_asm<D, C::BQ, NW>(d_o + row_base * D, q0, p.n_q, smem_base + C::do_off(slot), wave, lane);
     const int r = q0 + lane;
     const int rc = r < p.n_q ? r : p.n_q - 1;
     dma4(((wave & 1) ? dsum : lse) + row_base + rc,
@@ -281,12 +282,10 @@ __global__ void __launch_bounds__(256) bwd_main(cowa_params p, SchedView sv, con
       sb[hf][nt][4 * i + r] = (__bf16)(pv * (pacc[mt][nt][r] - dd));
     }
   };
-  auto load_rowv = [&](const float* rowv, int hf, float4 (&l4)[2], float4 (&d4)[2]) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      l4[i] = *reinterpret_cast<const float4*>(rowv + (2 * hf + i) * 16 + 4 * lg);
-      d4[i] = *reinterpret_cast<const float4*>(rowv + C::BQ + (2 * hf + i) * 16 + 4 * lg);
-    }
+  // LSE and D of query tile 2 hf + i (the lane's rows 4 lg .. 4 lg + 3)
+  auto load_rowv = [&](const float* rowv, int hf, int i, float4 (&l4)[2], float4 (&d4)[2]) {
+    l4[i] = *reinterpret_cast<const float4*>(rowv + (2 * hf + i) * 16 + 4 * lg);
+    d4[i] = *reinterpret_cast<const float4*>(rowv + C::BQ + (2 * hf + i) * 16 + 4 * lg);
   };
 
   int slot = 0;  // ring slot of the step being computed (t mod 3)
@@ -298,45 +297,48 @@ __global__ void __launch_bounds__(256) bwd_main(cowa_params p, SchedView sv, con
     const int q0 = (int)(entry_of(c_ph, c_k) >> 1) * p.tile_q + c_sub * C::BQ;
     stage(entry_of(n2_ph, n2_k), n2_hh, n2_sub, slot2);
 
-    bf16x8 fa[2], fb[2];  // operand fragments, one group ahead
+    // groups 0 .. 4 NG - 1: S/dP(half 0), S/dP(half 1), dV/dK(half 0), dV/dK(half 1);
+    // operand fragments are read PD groups ahead of their MFMAs
+    constexpr int NGT = 4 * NG, PD = 1;
+    auto load_group = [&](int gg, bf16x8& fa, bf16x8& fb) {
+      if (gg < NG)
+        sdp_load(qs, dos, 0, gg, fa, fb);
+      else if (gg < 2 * NG)
+        sdp_load(qs, dos, 1, gg - NG, fa, fb);
+      else if (gg < 3 * NG)
+        dvdk_load(qs, dos, 0, gg - 2 * NG, fa, fb);
+      else
+        dvdk_load(qs, dos, 1, gg - 3 * NG, fa, fb);
+    };
+    bf16x8 fa[PD + 1], fb[PD + 1];
     float4 l4[2], d4[2];  // LSE and D of the half in the softmax
-    sdp_load(qs, dos, 0, 0, fa[0], fb[0]);
+#pragma unroll
+    for (int gg = 0; gg < PD; ++gg) load_group(gg, fa[gg], fb[gg]);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int gi = 0; gi < NG; ++gi) {  // S/dP of half 0
-      if (gi + 1 < NG)
-        sdp_load(qs, dos, 0, gi + 1, fa[(gi + 1) & 1], fb[(gi + 1) & 1]);
+    for (int gg = 0; gg < NGT; ++gg) {
+      if (gg + PD < NGT) load_group(gg + PD, fa[(gg + PD) % (PD + 1)], fb[(gg + PD) % (PD + 1)]);
+      // the row values of a half's first and second query tile are needed by
+      // its softmax chunks [0, NG/2) and [NG/2, NG); each is loaded once the
+      // previous half no longer reads that register
+      if (gg == NG - 2) {
+        load_rowv(rowv, 0, 0, l4, d4);
+        load_rowv(rowv, 0, 1, l4, d4);
+      }
+      if (gg == NG + NG / 2) load_rowv(rowv, 1, 0, l4, d4);
+      if (gg == 2 * NG) load_rowv(rowv, 1, 1, l4, d4);
+      bf16x8& a0 = fa[gg % (PD + 1)];
+      bf16x8& b0 = fb[gg % (PD + 1)];
+      if (gg < NG)
+        sdp_mfma(0, gg, a0, b0);
+      else if (gg < 2 * NG)
+        sdp_mfma(1, gg - NG, a0, b0);
+      else if (gg < 3 * NG)
+        dvdk_mfma(0, gg - 2 * NG, a0, b0);
       else
-        sdp_load(qs, dos, 1, 0, fa[(gi + 1) & 1], fb[(gi + 1) & 1]);
-      if (gi == NG - 1) load_rowv(rowv, 0, l4, d4);
-      sdp_mfma(0, gi, fa[gi & 1], fb[gi & 1]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-#pragma unroll
-    for (int gi = 0; gi < NG; ++gi) {  // S/dP of half 1, softmax of half 0
-      if (gi + 1 < NG)
-        sdp_load(qs, dos, 1, gi + 1, fa[(gi + 1) & 1], fb[(gi + 1) & 1]);
-      else
-        dvdk_load(qs, dos, 0, 0, fa[(gi + 1) & 1], fb[(gi + 1) & 1]);
-      sdp_mfma(1, gi, fa[gi & 1], fb[gi & 1]);
-      soft_chunk(0, gi, l4, d4, masked, q0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    load_rowv(rowv, 1, l4, d4);
-#pragma unroll
-    for (int md = 0; md < C::MD; ++md) {  // dV/dK of half 0, softmax of half 1
-      if (md + 1 < C::MD)
-        dvdk_load(qs, dos, 0, md + 1, fa[(md + 1) & 1], fb[(md + 1) & 1]);
-      else
-        dvdk_load(qs, dos, 1, 0, fa[(md + 1) & 1], fb[(md + 1) & 1]);
-      dvdk_mfma(0, md, fa[md & 1], fb[md & 1]);
-      soft_chunk(1, md, l4, d4, masked, q0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-#pragma unroll
-    for (int md = 0; md < C::MD; ++md) {  // dV/dK of half 1
-      if (md + 1 < C::MD) dvdk_load(qs, dos, 1, md + 1, fa[(md + 1) & 1], fb[(md + 1) & 1]);
-      dvdk_mfma(1, md, fa[md & 1], fb[md & 1]);
+        dvdk_mfma(1, gg - 3 * NG, a0, b0);
+      if (gg >= NG && gg < 2 * NG) soft_chunk(0, gg - NG, l4, d4, masked, q0);
+      if (gg >= 2 * NG && gg < 3 * NG) soft_chunk(1, gg - 2 * NG, l4, d4, masked, q0);
       __builtin_amdgcn_sched_barrier(0);
     }
 
@@ -396,14 +398,14 @@ __global__ void __launch_bounds__(256) bwd_main(cowa_params p, SchedView sv, con
   }
 }
 
-template <int D, int BK>
+template <int D, int BK, int NW = 4>
 hipError_t launch_main(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
                        const void* d_o, const float* lse, const float* dsum, void* dk, void* dv,
                        hipStream_t stream) {
-  using C = BwdCfg<D, BK>;
+  using C = BwdCfg<D, BK, NW>;
   static_assert(C::OUT_BYTES <= C::LDS_MAX && C::MAIN_BYTES < C::LDS_MAX, "LDS budget");
   if (sv.n_qt > C::max_qblocks()) return hipErrorInvalidValue;
-  auto kern = bwd_main<D, BK>;
+  auto kern = bwd_main<D, BK, NW>;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -412,7 +414,7 @@ hipError_t launch_main(const cowa_params& p, const SchedView& sv, const void* q,
     attr_set = true;
   }
   const unsigned blocks = (unsigned)sv.n_kt * p.h_k * p.batch;
-  hipLaunchKernelGGL(kern, dim3(blocks), dim3(256), C::lds_bytes(sv.n_qt), stream, p, sv,
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * NW), C::lds_bytes(sv.n_qt), stream, p, sv,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), static_cast<const __bf16*>(v),
                      static_cast<const __bf16*>(d_o), lse, dsum, static_cast<__bf16*>(dk),
                      static_cast<__bf16*>(dv));
@@ -461,8 +463,8 @@ __global__ void __launch_bounds__(512) bwd_dq_kernel(cowa_params p, SchedView sv
   const int e0 = sv.fwd_row_ptr[r], e1 = sv.fwd_row_ptr[r + 1];
   if (e0 < e1) {
     const int64_t kf = (int64_t)(sv.fwd_ent[e0] >> 1) * BK;
-    load_tile_nw<D, BK>(kbase, (int)kf, p.n_k, smem, wave, nw, lane);
-    load_tile_nw<D, BK>(vbase, (int)kf, p.n_k, smem + T::BYTES, wave, nw, lane);
+    load_tile_asm_nw<D, BK>(kbase, (int)kf, p.n_k, lds_addr(smem), wave, nw, lane);
+    load_tile_asm_nw<D, BK>(vbase, (int)kf, p.n_k, lds_addr(smem) + T::BYTES, wave, nw, lane);
   }
 
   // Q^T and dO^T fragments (B operands): query column nt*16 + lr, d = ks*32 + 8*lg + 0..7;
@@ -498,17 +500,23 @@ __global__ void __launch_bounds__(512) bwd_dq_kernel(cowa_params p, SchedView sv
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
+  // schedule entries one and two blocks ahead are read early, so that no
+  // iteration waits on the load of the entry it prefetches
+  uint32_t ent_cur = e0 < e1 ? sv.fwd_ent[e0] : 0u;
+  uint32_t ent_nxt = e0 + 1 < e1 ? sv.fwd_ent[e0 + 1] : 0u;
   for (int e = e0; e < e1; ++e) {
     const int buf = (e - e0) & 1;
-    const uint32_t ent = sv.fwd_ent[e];
+    const uint32_t ent = ent_cur;
     const bool partial = ent & 1u;
     const int64_t k_first = (int64_t)(ent >> 1) * BK;
     if (e + 1 < e1) {
-      const int64_t kf = (int64_t)(sv.fwd_ent[e + 1] >> 1) * BK;
+      const int64_t kf = (int64_t)(ent_nxt >> 1) * BK;
       unsigned char* nb = smem + (buf ^ 1) * 2 * T::BYTES;
-      load_tile_nw<D, BK>(kbase, (int)kf, p.n_k, nb, wave, nw, lane);
-      load_tile_nw<D, BK>(vbase, (int)kf, p.n_k, nb + T::BYTES, wave, nw, lane);
+      load_tile_asm_nw<D, BK>(kbase, (int)kf, p.n_k, lds_addr(nb), wave, nw, lane);
+      load_tile_asm_nw<D, BK>(vbase, (int)kf, p.n_k, lds_addr(nb) + T::BYTES, wave, nw, lane);
     }
+    ent_cur = ent_nxt;
+    ent_nxt = sv.fwd_ent[e + 2 < e1 ? e + 2 : e1 - 1];  // unconditional: no merge of wait states
     const unsigned char* Kt = smem + buf * 2 * T::BYTES;
     const unsigned char* Vt = Kt + T::BYTES;
 

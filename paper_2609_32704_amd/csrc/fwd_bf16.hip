@@ -70,8 +70,8 @@ __global__ void __launch_bounds__(512) fwd_bf16_kernel(cowa_params p, SchedView 
   // buffer s: K at smem + 2 s BYTES, V right after it
   if (e0 < e1) {
     const int64_t kf = (int64_t)(sv.fwd_ent[e0] >> 1) * BK;
-    load_tile_nw<D, BK>(kbase, (int)kf, p.n_k, smem, wave, nw, lane);
-    load_tile_nw<D, BK>(vbase, (int)kf, p.n_k, smem + T::BYTES, wave, nw, lane);
+    load_tile_asm_nw<D, BK>(kbase, (int)kf, p.n_k, lds_addr(smem), wave, nw, lane);
+    load_tile_asm_nw<D, BK>(vbase, (int)kf, p.n_k, lds_addr(smem) + T::BYTES, wave, nw, lane);
   }
 
   // Q^T fragments (B operand): query column nt*16 + lr, d = ks*32 + 8*lg + 0..7
@@ -101,18 +101,24 @@ __global__ void __launch_bounds__(512) fwd_bf16_kernel(cowa_params p, SchedView 
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
+  // schedule entries one and two blocks ahead are read early, so that no
+  // iteration waits on the load of the entry it prefetches
+  uint32_t ent_cur = e0 < e1 ? sv.fwd_ent[e0] : 0u;
+  uint32_t ent_nxt = e0 + 1 < e1 ? sv.fwd_ent[e0 + 1] : 0u;
   for (int e = e0; e < e1; ++e) {
     const int buf = (e - e0) & 1;
-    const uint32_t ent = sv.fwd_ent[e];
+    const uint32_t ent = ent_cur;
     const int j = (int)(ent >> 1);
     const bool partial = ent & 1u;
     const int64_t k_first = (int64_t)j * BK;
     if (e + 1 < e1) {  // prefetch the next block into the other buffer
-      const int64_t kf = (int64_t)(sv.fwd_ent[e + 1] >> 1) * BK;
+      const int64_t kf = (int64_t)(ent_nxt >> 1) * BK;
       unsigned char* nb = smem + (buf ^ 1) * 2 * T::BYTES;
-      load_tile_nw<D, BK>(kbase, (int)kf, p.n_k, nb, wave, nw, lane);
-      load_tile_nw<D, BK>(vbase, (int)kf, p.n_k, nb + T::BYTES, wave, nw, lane);
+      load_tile_asm_nw<D, BK>(kbase, (int)kf, p.n_k, lds_addr(nb), wave, nw, lane);
+      load_tile_asm_nw<D, BK>(vbase, (int)kf, p.n_k, lds_addr(nb) + T::BYTES, wave, nw, lane);
     }
+    ent_cur = ent_nxt;
+    ent_nxt = sv.fwd_ent[e + 2 < e1 ? e + 2 : e1 - 1];  // unconditional: no merge of wait states
     const unsigned char* Kt = smem + buf * 2 * T::BYTES;
     const unsigned char* Vt = Kt + T::BYTES;
 

@@ -128,6 +128,28 @@ __device__ inline void load_tile_asm(const __bf16* base, int first, int n_rows, 
   }
 }
 
+// load_tile_asm for a wave-uniform wave count known at run time.
+template <int D, int ROWS>
+__device__ inline void load_tile_asm_nw(const __bf16* base, int first, int n_rows, uint32_t lds, int wave, int nw,
+                                        int lane) {
+  using T = SwzTile<D, ROWS>;
+  constexpr int RPL = 1024 / (D * 2);
+  if constexpr (T::LOADS % 8 == 0 && (8 * RPL) % 16 == 0) {
+    if (nw == 8) return load_tile_asm<D, ROWS, 8>(base, first, n_rows, lds, wave, lane);
+  }
+  if constexpr (T::LOADS % 4 == 0 && (4 * RPL) % 16 == 0) {
+    if (nw == 4) return load_tile_asm<D, ROWS, 4>(base, first, n_rows, lds, wave, lane);
+  }
+  for (int n = wave; n < T::LOADS; n += nw) {
+    const int flat = n * 64 + lane;
+    const int row = flat / T::CH, slot = flat % T::CH;
+    const int chunk = slot ^ swz<T::CH>(row);
+    int r = first + row;
+    r = r < n_rows ? r : n_rows - 1;
+    dma16(base + (int64_t)r * D + chunk * 8, __builtin_amdgcn_readfirstlane(lds + n * 1024));
+  }
+}
+
 // The same for any wave count (a lane's chunk recomputed per piece).
 template <int D, int ROWS>
 __device__ inline void load_tile_any(const __bf16* base, int first, int n_rows, unsigned char* lds, int wave, int nw,
