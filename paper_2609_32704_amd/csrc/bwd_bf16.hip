@@ -422,22 +422,42 @@ hipError_t launch_main(const cowa_params& p, const SchedView& sv, const void* q,
 }
 
 // dQ pass: one workgroup per (QO block i, HPW QO heads of one KV group,
-// sequence b); each 64-lane wave owns 32 query rows of one head.
+// sequence b); each 64-lane wave owns 64 query rows of one head, and one wave
+// runs per SIMD.  Q^T and dO^T of the wave's rows stay in registers (as MFMA B
+// operands, pinned to AGPRs) for the whole row of KV blocks; K_j and V_j are
+// double buffered in LDS and shared by the heads.  Full blocks are taken first,
+// then partial ones (each kind a straight-line loop body).  Per chunk of 32 keys:
+//   phase A: S^T = K Q^T and dP^T = V dO^T for 16 keys (32 MFMAs),
+//   phase B: dS^T = P^T (dP^T - D) for those keys on the vector units while the
+//            matrix cores run half of dQ^T += K^T dS^T of the previous chunk,
+// twice per chunk;
+// the softmax scale is applied to dQ when it is written.
 template <int D, int BQ, int BK>
-__global__ void __launch_bounds__(512) bwd_dq_kernel(cowa_params p, SchedView sv, int hpw, int n_hgroups,
+struct DqCfg {
+  static constexpr int NQW = 64;            // query rows per wave
+  static constexpr int NTQ = NQW / 16;      // query tiles per wave
+  static constexpr int BKC = 32;            // keys per chunk (one k-step of dQ^T += K^T dS^T)
+  static constexpr int MTK = 1;             // S^T and dP^T are computed 16 keys (one key tile) at a time
+  static constexpr int NCH = BK / BKC;      // chunks per block
+  static constexpr int KSD = D / 32;        // k-steps over d
+  static constexpr int MTD = D / 16;        // d tiles of dQ^T
+  static constexpr int WPH = BQ / NQW;      // waves per QO head
+  using T = SwzTile<D, BK>;
+  static constexpr int MAIN_BYTES = 4 * T::BYTES;  // K, V of two blocks; then the row's entry lists
+  static constexpr int LDS_MAX = 160 * 1024;
+  static int lds_bytes(int n_kt) { return MAIN_BYTES + 4 * n_kt; }
+  static int max_kblocks() { return (LDS_MAX - MAIN_BYTES) / 4; }
+};
+
+template <int D, int BQ, int BK>
+__global__ void __launch_bounds__(256) bwd_dq_kernel(cowa_params p, SchedView sv, int hpw, int n_hgroups,
                                                      const __bf16* __restrict__ q, const __bf16* __restrict__ k,
                                                      const __bf16* __restrict__ v, const __bf16* __restrict__ d_o,
                                                      const float* __restrict__ lse, const float* __restrict__ dsum,
                                                      __bf16* __restrict__ dq) {
-  using T = SwzTile<D, BK>;
-  constexpr int NQW = 32;                 // query rows per wave
-  constexpr int NTQ = NQW / 16;           // query tiles per wave
-  constexpr int BKC = D > 64 ? 32 : 64;   // keys per step (register budget of two waves per SIMD)
-  constexpr int MTK = BKC / 16;           // key tiles of S^T
-  constexpr int KSD = D / 32;             // k-steps over d
-  constexpr int MTD = D / 16;             // d tiles of dQ^T
-  constexpr int KSK = BKC / 32;           // k-steps over keys
-  constexpr int WAVES_PER_HEAD = BQ / NQW;
+  using C = DqCfg<D, BQ, BK>;
+  using T = typename C::T;
+  constexpr int NTQ = C::NTQ, MTK = C::MTK, KSD = C::KSD, MTD = C::MTD;
   extern __shared__ __align__(1024) unsigned char smem[];
 
   const int nw = blockDim.x >> 6;
@@ -453,28 +473,57 @@ __global__ void __launch_bounds__(512) bwd_dq_kernel(cowa_params p, SchedView sv
 
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int lr = lane & 15, lg = lane >> 4;
-  const int h = h0 + wave / WAVES_PER_HEAD;
-  const int64_t q_first = (int64_t)i * BQ + (wave % WAVES_PER_HEAD) * NQW;
+  const int h = h0 + wave / C::WPH;
+  const int q_first = i * BQ + (wave % C::WPH) * C::NQW;
   const Geo32 g = geo32(make_geo(p.n_q, p.n_k, p.w_sink, p.w_near, BQ, BK, p.h_k_offset + hk, p.h_k_total));
 
   const __bf16* kbase = k + ((int64_t)b * p.h_k + hk) * p.n_k * D;
   const __bf16* vbase = v + ((int64_t)b * p.h_k + hk) * p.n_k * D;
+  const uint32_t smem_base = lds_addr(smem);
+
+  // the row's entries, split into full (from the front) and partial (from the back) lists
   const int r = hk * sv.n_qt + i;
   const int e0 = sv.fwd_row_ptr[r], e1 = sv.fwd_row_ptr[r + 1];
-  if (e0 < e1) {
-    const int64_t kf = (int64_t)(sv.fwd_ent[e0] >> 1) * BK;
-    load_tile_asm_nw<D, BK>(kbase, (int)kf, p.n_k, lds_addr(smem), wave, nw, lane);
-    load_tile_asm_nw<D, BK>(vbase, (int)kf, p.n_k, lds_addr(smem) + T::BYTES, wave, nw, lane);
+  const int n_ent = e1 - e0;
+  const int cap = sv.n_kt;
+  uint32_t* list = reinterpret_cast<uint32_t*>(smem + C::MAIN_BYTES);
+  int n_full = 0;
+  for (int c0 = 0; c0 < n_ent; c0 += 64) {
+    const bool in = c0 + lane < n_ent;
+    const uint32_t ent = in ? sv.fwd_ent[e0 + c0 + lane] : 0u;
+    const uint64_t full = __ballot(in && !(ent & 1u));
+    const uint64_t part = __ballot(in && (ent & 1u));
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    if (wave == 0 && in) {
+      if (ent & 1u)
+        list[cap - 1 - (c0 - n_full + __popcll(part & below))] = ent;
+      else
+        list[n_full + __popcll(full & below)] = ent;
+    }
+    n_full += __popcll(full);
   }
+  // list position of the t-th block in processing order (full ones, then partial ones)
+  auto entry_at = [&](int t) -> uint32_t {
+    const int tt = t < n_ent ? t : n_ent - 1;
+    const int idx = tt < n_full ? tt : cap - 1 - (tt - n_full);
+    return __builtin_amdgcn_readfirstlane(list[idx]);
+  };
+  auto stage = [&](uint32_t ent, int buf) {
+    const int kf = (int)(ent >> 1) * BK;
+    load_tile_asm_nw<D, BK>(kbase, kf, p.n_k, smem_base + buf * 2 * T::BYTES, wave, nw, lane);
+    load_tile_asm_nw<D, BK>(vbase, kf, p.n_k, smem_base + buf * 2 * T::BYTES + T::BYTES, wave, nw, lane);
+  };
+  __syncthreads();  // the lists are in LDS
+  if (n_ent > 0) stage(entry_at(0), 0);
 
   // Q^T and dO^T fragments (B operands): query column nt*16 + lr, d = ks*32 + 8*lg + 0..7;
-  // per-query LSE (base 2; an empty row gets +inf so that P = 0) and D
+  // per-query LSE (base 2; a row without keys or past n_q gets +inf, so P = 0) and D
   const int64_t row_base = ((int64_t)b * p.h_q + h) * p.n_q;
   bf16x8 qf[NTQ][KSD], gf[NTQ][KSD];
   float l2[NTQ], dd[NTQ];
 #pragma unroll
   for (int nt = 0; nt < NTQ; ++nt) {
-    const int64_t qp = q_first + nt * 16 + lr;
+    const int qp = q_first + nt * 16 + lr;
     const bool ok = qp < p.n_q;
     const int64_t row = row_base + (ok ? qp : 0);
 #pragma unroll
@@ -489,111 +538,119 @@ __global__ void __launch_bounds__(512) bwd_dq_kernel(cowa_params p, SchedView sv
     dd[nt] = ok ? dsum[row] : 0.f;
   }
 
-  f32x4 qacc[MTD][NTQ];  // dQ^T: rows d, columns queries
+  f32x4 qacc[MTD][NTQ];  // dQ^T / scale: rows d, columns queries
 #pragma unroll
   for (int md = 0; md < MTD; ++md)
 #pragma unroll
     for (int nt = 0; nt < NTQ; ++nt) qacc[md][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
   const float c = p.softmax_scale * kLog2e;
-  const float scale = p.softmax_scale;
+  // per-lane offsets: K/V row fragments (row lr of a 16-row tile, chunk 4 ks + lg)
+  // and the transposing K^T reads (rows 4 lg + lr / 4, column 16 md + 4 (lr % 4))
+  int offr[KSD], offt[MTD];
+#pragma unroll
+  for (int ks = 0; ks < KSD; ++ks) offr[ks] = row8_off<D>(lr, lg, ks);
+#pragma unroll
+  for (int md = 0; md < MTD; ++md) offt[md] = tr8_off<D>(lr, lg, md);
 
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
-  // schedule entries one and two blocks ahead are read early, so that no
-  // iteration waits on the load of the entry it prefetches
-  uint32_t ent_cur = e0 < e1 ? sv.fwd_ent[e0] : 0u;
-  uint32_t ent_nxt = e0 + 1 < e1 ? sv.fwd_ent[e0 + 1] : 0u;
-  for (int e = e0; e < e1; ++e) {
-    const int buf = (e - e0) & 1;
-    const uint32_t ent = ent_cur;
-    const bool partial = ent & 1u;
-    const int64_t k_first = (int64_t)(ent >> 1) * BK;
-    if (e + 1 < e1) {
-      const int64_t kf = (int64_t)(ent_nxt >> 1) * BK;
-      unsigned char* nb = smem + (buf ^ 1) * 2 * T::BYTES;
-      load_tile_asm_nw<D, BK>(kbase, (int)kf, p.n_k, lds_addr(nb), wave, nw, lane);
-      load_tile_asm_nw<D, BK>(vbase, (int)kf, p.n_k, lds_addr(nb) + T::BYTES, wave, nw, lane);
-    }
-    ent_cur = ent_nxt;
-    ent_nxt = sv.fwd_ent[e + 2 < e1 ? e + 2 : e1 - 1];  // unconditional: no merge of wait states
-    const unsigned char* Kt = smem + buf * 2 * T::BYTES;
-    const unsigned char* Vt = Kt + T::BYTES;
+  f32x4 sacc[NTQ], pacc[NTQ];  // S^T, dP^T of 16 keys: rows keys 4 lg + rr, column query 16 nt + lr
+  bf16x8 sb[2][NTQ];           // dS^T of the current and the previous chunk as B operands
 
-#pragma unroll 1
-    for (int kc = 0; kc < BK; kc += BKC) {
-      // S^T = K Q^T and dP^T = V dO^T: rows keys kc + mt*16 + 4*lg + rr, column query nt*16 + lr
-      f32x4 sacc[MTK][NTQ], pacc[MTK][NTQ];
+  // phase A: S^T and dP^T of key tile kt (keys 16 kt .. 16 kt + 15 of the block)
+  auto phase_a = [&](const unsigned char* Kt, const unsigned char* Vt, int kt) {
 #pragma unroll
-      for (int mt = 0; mt < MTK; ++mt)
-#pragma unroll
-        for (int nt = 0; nt < NTQ; ++nt) {
-          sacc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-          pacc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-#pragma unroll
-      for (int ks = 0; ks < KSD; ++ks)
-#pragma unroll
-        for (int mt = 0; mt < MTK; ++mt) {
-          const bf16x8 ak = read_row8<D, BK>(Kt, kc + mt * 16 + lr, ks * 4 + lg);
-          const bf16x8 av = read_row8<D, BK>(Vt, kc + mt * 16 + lr, ks * 4 + lg);
-#pragma unroll
-          for (int nt = 0; nt < NTQ; ++nt) {
-            sacc[mt][nt] = mfma16(ak, qf[nt][ks], sacc[mt][nt]);
-            pacc[mt][nt] = mfma16(av, gf[nt][ks], pacc[mt][nt]);
-          }
-        }
-
-      // P^T = exp(S^T - LSE), scale dS^T = scale P^T (dP^T - D); masked pairs: an
-      // additive -inf in the exponent (an update that reads the MFMA result)
-      const int k0 = (int)k_first + kc + 4 * lg;
+    for (int ks = 0; ks < KSD; ++ks) {
+      const int rowoff = kt * 16 * D * 2;
+      const bf16x8 ak = ld_row8(Kt + offr[ks] + rowoff);
+      const bf16x8 av = ld_row8(Vt + offr[ks] + rowoff);
 #pragma unroll
       for (int nt = 0; nt < NTQ; ++nt) {
-        const int qp = (int)q_first + nt * 16 + lr;
-#pragma unroll
-        for (int mt = 0; mt < MTK; ++mt)
-#pragma unroll
-          for (int rr = 0; rr < 4; ++rr) {
-            const float bias = (!partial || legal32(g, qp, k0 + mt * 16 + rr)) ? 0.f : -INFINITY;
-            const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[mt][nt][rr], c, -l2[nt]) + bias);
-            sacc[mt][nt][rr] = scale * pv * (pacc[mt][nt][rr] - dd[nt]);
-          }
+        sacc[nt] = mfma16(ak, qf[nt][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sacc[nt]);
+        pacc[nt] = mfma16(av, gf[nt][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : pacc[nt]);
       }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  // dS^T of key tile kt, query tile nt into sb[sl], k-slots 4 (kt % 2) + rr
+  // (key 16 kt + 4 lg + rr of the block); the chunk's k-slot order is the one
+  // the transposing K^T read produces
+  auto ds_tile = [&](int sl, int kt, int nt, bool masked, int k_first) {
+    const int qp = q_first + nt * 16 + lr;
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      float x = fmaf(sacc[nt][rr], c, -l2[nt]);
+      if (masked) x = legal32(g, qp, k_first + kt * 16 + 4 * lg + rr) ? x : -INFINITY;
+      const float pv = __builtin_amdgcn_exp2f(x);
+      sb[sl][nt][4 * (kt & 1) + rr] = (__bf16)(pv * (pacc[nt][rr] - dd[nt]));
+    }
+  };
+  // dQ^T += K^T dS^T for chunk kc (from sb[sl]), d tile md
+  auto dq_mfma = [&](const unsigned char* Kt, int kc, int sl, int md) {
+    const bf16x8 a = ld_tr8(Kt + offt[md] + kc * C::BKC * D * 2, D * 2);
+#pragma unroll
+    for (int nt = 0; nt < NTQ; ++nt) qacc[md][nt] = mfma16(a, sb[sl][nt], qacc[md][nt]);
+  };
 
-      // dQ^T += K^T (scale dS^T): k-slots are keys kc + 32ks + 4lg + t and kc + 32ks + 16 + 4lg + t
+  auto block = [&](int t, bool masked) {
+    const int buf = t & 1;
+    const uint32_t ent = entry_at(t);
+    const int k_first = (int)(ent >> 1) * BK;
+    if (t + 1 < n_ent) stage(entry_at(t + 1), buf ^ 1);  // prefetch the next block
+    const unsigned char* Kt = smem + buf * 2 * T::BYTES;
+    const unsigned char* Vt = Kt + T::BYTES;
 #pragma unroll
-      for (int ks = 0; ks < KSK; ++ks) {
-        bf16x8 sb[NTQ];
+    for (int kc = 0; kc < C::NCH; ++kc) {
 #pragma unroll
-        for (int nt = 0; nt < NTQ; ++nt)
+      for (int hf = 0; hf < 2; ++hf) {
+        const int kt = 2 * kc + hf;
+        phase_a(Kt, Vt, kt);
+        // phase B: dS^T of this key tile (NTQ pieces) interleaved with half of
+        // dQ^T of the previous chunk (MTD / 2 d tiles)
 #pragma unroll
-          for (int rr = 0; rr < 4; ++rr) {
-            sb[nt][rr] = (__bf16)sacc[2 * ks][nt][rr];
-            sb[nt][4 + rr] = (__bf16)sacc[2 * ks + 1][nt][rr];
-          }
+        for (int x = 0; x < MTD / 2; ++x) {
+          if (kc > 0) dq_mfma(Kt, kc - 1, (kc - 1) & 1, hf * (MTD / 2) + x);
 #pragma unroll
-        for (int md = 0; md < MTD; ++md) {
-          const bf16x8 a = read_tr8<D, BK>(Kt, kc + ks * 32, md * 16, lr, lg);
-#pragma unroll
-          for (int nt = 0; nt < NTQ; ++nt) qacc[md][nt] = mfma16(a, sb[nt], qacc[md][nt]);
+          for (int nt = x * NTQ / (MTD / 2); nt < (x + 1) * NTQ / (MTD / 2); ++nt)
+            ds_tile(kc & 1, kt, nt, masked, k_first);
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
     }
+#pragma unroll
+    for (int md = 0; md < MTD; ++md) {  // dQ^T of the last chunk
+      dq_mfma(Kt, C::NCH - 1, (C::NCH - 1) & 1, md);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // register placement: dQ^T accumulators in VGPRs, Q^T / dO^T fragments in
+    // AGPRs (read directly as B operands); these statements emit nothing
+#pragma unroll
+    for (int md = 0; md < MTD; ++md)
+#pragma unroll
+      for (int nt = 0; nt < NTQ; ++nt) asm volatile("" : "+v"(qacc[md][nt]));
+#pragma unroll
+    for (int nt = 0; nt < NTQ; ++nt)
+#pragma unroll
+      for (int ks = 0; ks < KSD; ++ks) asm volatile("" : "+a"(qf[nt][ks]), "+a"(gf[nt][ks]));
+    __builtin_amdgcn_s_waitcnt(0);  // the next block has landed
+    __syncthreads();                 // ... for every wave, and this block is no longer read
+  };
+  int t = 0;
+  for (; t < n_full; ++t) block(t, false);
+  for (; t < n_ent; ++t) block(t, true);
 
-    __builtin_amdgcn_s_waitcnt(0);  // the prefetch of block e+1 has landed
-    __syncthreads();                 // ... for every wave, and block e is no longer read
-  }
-
+  const float scale = p.softmax_scale;
 #pragma unroll
   for (int nt = 0; nt < NTQ; ++nt) {
-    const int64_t qp = q_first + nt * 16 + lr;
+    const int qp = q_first + nt * 16 + lr;
     if (qp >= p.n_q) continue;
     __bf16* drow = dq + (row_base + qp) * D;
 #pragma unroll
     for (int md = 0; md < MTD; ++md) {
       bf16x4 w4;
 #pragma unroll
-      for (int rr = 0; rr < 4; ++rr) w4[rr] = (__bf16)qacc[md][nt][rr];
+      for (int rr = 0; rr < 4; ++rr) w4[rr] = (__bf16)(scale * qacc[md][nt][rr]);
       *reinterpret_cast<bf16x4*>(drow + md * 16 + 4 * lg) = w4;
     }
   }
@@ -602,23 +659,23 @@ __global__ void __launch_bounds__(512) bwd_dq_kernel(cowa_params p, SchedView sv
 template <int D, int BQ, int BK>
 hipError_t launch_dq(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
                      const void* d_o, const float* lse, const float* dsum, void* dq, hipStream_t stream) {
-  constexpr int LDS = 4 * SwzTile<D, BK>::BYTES;
-  static_assert(LDS <= 160 * 1024, "LDS budget");
+  using C = DqCfg<D, BQ, BK>;
+  if (sv.n_kt > C::max_kblocks()) return hipErrorInvalidValue;
   auto kern = bwd_dq_kernel<D, BQ, BK>;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_MAX);
     if (err != hipSuccess) return err;
     attr_set = true;
   }
   const int G = p.h_q / p.h_k;
-  int hpw = 256 / BQ;  // up to 256 query rows per workgroup
+  int hpw = 256 / BQ;  // up to 256 query rows (four waves) per workgroup
   while (hpw > 1 && G % hpw != 0) hpw >>= 1;
   const int n_hgroups = p.h_q / hpw;
-  const int waves = hpw * (BQ / 32);
+  const int waves = hpw * C::WPH;
   const unsigned blocks = (unsigned)sv.n_qt * n_hgroups * p.batch;
-  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * waves), LDS, stream, p, sv, hpw, n_hgroups,
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * waves), C::lds_bytes(sv.n_kt), stream, p, sv, hpw, n_hgroups,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), static_cast<const __bf16*>(v),
                      static_cast<const __bf16*>(d_o), lse, dsum, static_cast<__bf16*>(dq));
   return hipGetLastError();
