@@ -593,6 +593,54 @@ __global__ void __launch_bounds__(256) bwd_dq_kernel(cowa_params p, SchedView sv
     for (int nt = 0; nt < NTQ; ++nt) qacc[md][nt] = mfma16(a, sb[sl][nt], qacc[md][nt]);
   };
 
+  // A block is a fixed sequence of groups, each an LDS read (issued PD groups
+  // ahead) and the MFMAs that consume it:
+  //   per key tile kt (16 keys): KSD groups of S^T/dP^T, then MTD/2 groups of
+  //   dQ^T for the previous 32-key chunk interleaved with dS^T of tile kt;
+  //   finally MTD groups of dQ^T for the last chunk.
+  constexpr int GPS = KSD + MTD / 2, NKT = 2 * C::NCH, NGB = NKT * GPS + MTD, PD = 1;
+  auto load_g = [&](const unsigned char* Kt, const unsigned char* Vt, int gg, bf16x8& fa, bf16x8& fb) {
+    if (gg < NKT * GPS) {
+      const int kt = gg / GPS, r = gg % GPS;
+      if (r < KSD) {
+        fa = ld_row8(Kt + offr[r] + kt * 16 * D * 2);
+        fb = ld_row8(Vt + offr[r] + kt * 16 * D * 2);
+      } else if (kt >= 2) {
+        const int md = (kt & 1) * (MTD / 2) + (r - KSD);
+        fa = ld_tr8(Kt + offt[md] + (kt / 2 - 1) * C::BKC * D * 2, D * 2);
+      }
+    } else {
+      const int md = gg - NKT * GPS;
+      fa = ld_tr8(Kt + offt[md] + (C::NCH - 1) * C::BKC * D * 2, D * 2);
+    }
+  };
+  auto exec_g = [&](int gg, const bf16x8& fa, const bf16x8& fb, bool masked, int k_first) {
+    if (gg < NKT * GPS) {
+      const int kt = gg / GPS, r = gg % GPS;
+      if (r < KSD) {
+#pragma unroll
+        for (int nt = 0; nt < NTQ; ++nt) {
+          sacc[nt] = mfma16(fa, qf[nt][r], r == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sacc[nt]);
+          pacc[nt] = mfma16(fb, gf[nt][r], r == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : pacc[nt]);
+        }
+      } else {
+        const int x = r - KSD;
+        if (kt >= 2) {
+          const int md = (kt & 1) * (MTD / 2) + x, sl = (kt / 2 - 1) & 1;
+#pragma unroll
+          for (int nt = 0; nt < NTQ; ++nt) qacc[md][nt] = mfma16(fa, sb[sl][nt], qacc[md][nt]);
+        }
+#pragma unroll
+        for (int nt = x * NTQ / (MTD / 2); nt < (x + 1) * NTQ / (MTD / 2); ++nt)
+          ds_tile((kt / 2) & 1, kt, nt, masked, k_first);
+      }
+    } else {
+      const int md = gg - NKT * GPS, sl = (C::NCH - 1) & 1;
+#pragma unroll
+      for (int nt = 0; nt < NTQ; ++nt) qacc[md][nt] = mfma16(fa, sb[sl][nt], qacc[md][nt]);
+    }
+  };
+
   auto block = [&](int t, bool masked) {
     const int buf = t & 1;
     const uint32_t ent = entry_at(t);
@@ -600,29 +648,15 @@ __global__ void __launch_bounds__(256) bwd_dq_kernel(cowa_params p, SchedView sv
     if (t + 1 < n_ent) stage(entry_at(t + 1), buf ^ 1);  // prefetch the next block
     const unsigned char* Kt = smem + buf * 2 * T::BYTES;
     const unsigned char* Vt = Kt + T::BYTES;
-#pragma unroll
-    for (int kc = 0; kc < C::NCH; ++kc) {
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-        const int kt = 2 * kc + hf;
-        phase_a(Kt, Vt, kt);
-        // phase B: dS^T of this key tile (NTQ pieces) interleaved with half of
-        // dQ^T of the previous chunk (MTD / 2 d tiles)
-#pragma unroll
-        for (int x = 0; x < MTD / 2; ++x) {
-          if (kc > 0) dq_mfma(Kt, kc - 1, (kc - 1) & 1, hf * (MTD / 2) + x);
-#pragma unroll
-          for (int nt = x * NTQ / (MTD / 2); nt < (x + 1) * NTQ / (MTD / 2); ++nt)
-            ds_tile(kc & 1, kt, nt, masked, k_first);
-          __builtin_amdgcn_sched_barrier(0);
-        }
-      }
-    }
-#pragma unroll
-    for (int md = 0; md < MTD; ++md) {  // dQ^T of the last chunk
-      dq_mfma(Kt, C::NCH - 1, (C::NCH - 1) & 1, md);
+    bf16x8 fa[PD + 1], fb[PD + 1];
+    static_for<PD>([&](auto ic) { load_g(Kt, Vt, ic.value, fa[ic.value], fb[ic.value]); });
+    __builtin_amdgcn_sched_barrier(0);
+    static_for<NGB>([&](auto ic) {
+      constexpr int gg = decltype(ic)::value;
+      if constexpr (gg + PD < NGB) load_g(Kt, Vt, gg + PD, fa[(gg + PD) % (PD + 1)], fb[(gg + PD) % (PD + 1)]);
+      exec_g(gg, fa[gg % (PD + 1)], fb[gg % (PD + 1)], masked, k_first);
       __builtin_amdgcn_sched_barrier(0);
-    }
+    });
     // register placement: dQ^T accumulators in VGPRs, Q^T / dO^T fragments in
     // AGPRs (read directly as B operands); these statements emit nothing
 #pragma unroll

@@ -18,6 +18,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+#include <utility>
+
 namespace cowa {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -239,6 +242,17 @@ __device__ inline bf16x8 ld_tr8(const unsigned char* p, int row_bytes) {
 // operations are outstanding and leaves the other counters alone (gfx9 layout:
 // vmcnt bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
 constexpr int vmcnt_only(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+// f(std::integral_constant<int, I>) for I = 0 .. N-1, expanded at compile time
+// (a fixed instruction schedule whose steps differ by their index).
+template <class F, int... I>
+__device__ inline void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ inline void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 
 __device__ inline f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
