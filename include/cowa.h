@@ -154,7 +154,13 @@ cowa_status cowa_bwd_workspace_size(const cowa_params* p, size_t* bytes);
  * V, using the saved O and LSE of the forward.  dq like q; dk/dv like k/v
  * (keys that no query sees get zero).  bf16 only; tile_q and tile_k in
  * {64, 128}.  Equivalent to cowa_bwd_prepare, cowa_bwd_main and cowa_bwd_dq in
- * that order on the same workspace.  Deterministic: no atomics. */
+ * that order on the same workspace.  Deterministic: no atomics.
+ * Each pass keeps one schedule row or column in LDS, which bounds the shape:
+ * COWA_ERR_UNSUPPORTED (before any launch) when ceil(N_q / tile_q) exceeds
+ * 16000 (head_dim 128; 28288 for 64) or ceil(N_k / tile_k) exceeds 8192
+ * (head_dim 128, tile_k 128; 24576 for tile_k 64; 24576 and 32768 for
+ * head_dim 64): 2M query and 1M key tokens at the 128 x 128 tiles.  All
+ * three backward entry points apply these checks. */
 cowa_status cowa_bwd(const cowa_params* p, const cowa_schedule_t* s,
                      const void* q, const void* k, const void* v,
                      const void* o, const float* lse, const void* d_o,

@@ -260,6 +260,15 @@ static cowa_status check_bwd(const cowa_params* p, size_t ws_bytes, void* worksp
   if (!cowa::bwd_bf16_supported(p->head_dim, p->tile_q, p->tile_k))
     return fail(COWA_ERR_UNSUPPORTED, "bf16 backward is built for tile_q, tile_k in {64, 128} (got %d x %d)",
                 p->tile_q, p->tile_k);
+  // the dK/dV pass keeps a column's block list, the dQ pass a row's, in LDS
+  const int64_t n_qt = ((int64_t)p->n_q + p->tile_q - 1) / p->tile_q;
+  const int64_t n_kt = ((int64_t)p->n_k + p->tile_k - 1) / p->tile_k;
+  if (n_qt > cowa::bwd_main_max_qblocks(p->head_dim, p->tile_k))
+    return fail(COWA_ERR_UNSUPPORTED, "backward supports at most %d query blocks (got %lld)",
+                cowa::bwd_main_max_qblocks(p->head_dim, p->tile_k), (long long)n_qt);
+  if (n_kt > cowa::bwd_dq_max_kblocks(p->head_dim, p->tile_k))
+    return fail(COWA_ERR_UNSUPPORTED, "backward supports at most %d key blocks (got %lld)",
+                cowa::bwd_dq_max_kblocks(p->head_dim, p->tile_k), (long long)n_kt);
   size_t need = 0;
   COWA_TRY(cowa_bwd_workspace_size(p, &need));
   if (p->batch > 0 && (!workspace || ws_bytes < need || !aligned(workspace, 256)))
@@ -300,9 +309,6 @@ cowa_status cowa_bwd_main(const cowa_params* p, const cowa_schedule_t* s, const 
   COWA_TRY(check_tensor(dv, "dv", 16));
   if ((int64_t)s->n_kt * p->h_k * p->batch >= (int64_t(1) << 31))
     return fail(COWA_ERR_UNSUPPORTED, "too many key blocks for one launch");
-  if (s->n_qt > cowa::bwd_main_max_qblocks(p->head_dim, p->tile_k))
-    return fail(COWA_ERR_UNSUPPORTED, "backward dK/dV pass supports at most %d query blocks (got %d)",
-                cowa::bwd_main_max_qblocks(p->head_dim, p->tile_k), s->n_qt);
   COWA_TRY(check_device());
   return hip_status(cowa::launch_bwd_main(*p, cowa::sched_view(s), q, k, v, lse, d_o, dk, dv, dsum,
                                           static_cast<hipStream_t>(stream)),

@@ -432,9 +432,9 @@ hipError_t launch_main(const cowa_params& p, const SchedView& sv, const void* q,
 //            matrix cores run half of dQ^T += K^T dS^T of the previous chunk,
 // twice per chunk;
 // the softmax scale is applied to dQ when it is written.
-template <int D, int BQ, int BK>
+template <int D, int BQ, int BK, int NQW_ = 64>
 struct DqCfg {
-  static constexpr int NQW = 64;            // query rows per wave
+  static constexpr int NQW = NQW_;          // query rows per wave
   static constexpr int NTQ = NQW / 16;      // query tiles per wave
   static constexpr int BKC = 32;            // keys per chunk (one k-step of dQ^T += K^T dS^T)
   static constexpr int MTK = 1;             // S^T and dP^T are computed 16 keys (one key tile) at a time
@@ -449,13 +449,13 @@ struct DqCfg {
   static int max_kblocks() { return (LDS_MAX - MAIN_BYTES) / 4; }
 };
 
-template <int D, int BQ, int BK>
-__global__ void __launch_bounds__(256) bwd_dq_kernel(cowa_params p, SchedView sv, int hpw, int n_hgroups,
+template <int D, int BQ, int BK, int NQW>
+__global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, SchedView sv, int hpw, int n_hgroups,
                                                      const __bf16* __restrict__ q, const __bf16* __restrict__ k,
                                                      const __bf16* __restrict__ v, const __bf16* __restrict__ d_o,
                                                      const float* __restrict__ lse, const float* __restrict__ dsum,
                                                      __bf16* __restrict__ dq) {
-  using C = DqCfg<D, BQ, BK>;
+  using C = DqCfg<D, BQ, BK, NQW>;
   using T = typename C::T;
   constexpr int NTQ = C::NTQ, MTK = C::MTK, KSD = C::KSD, MTD = C::MTD;
   extern __shared__ __align__(1024) unsigned char smem[];
@@ -690,12 +690,12 @@ __global__ void __launch_bounds__(256) bwd_dq_kernel(cowa_params p, SchedView sv
   }
 }
 
-template <int D, int BQ, int BK>
+template <int D, int BQ, int BK, int NQW = 64>
 hipError_t launch_dq(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
                      const void* d_o, const float* lse, const float* dsum, void* dq, hipStream_t stream) {
-  using C = DqCfg<D, BQ, BK>;
+  using C = DqCfg<D, BQ, BK, NQW>;
   if (sv.n_kt > C::max_kblocks()) return hipErrorInvalidValue;
-  auto kern = bwd_dq_kernel<D, BQ, BK>;
+  auto kern = bwd_dq_kernel<D, BQ, BK, NQW>;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -704,7 +704,7 @@ hipError_t launch_dq(const cowa_params& p, const SchedView& sv, const void* q, c
     attr_set = true;
   }
   const int G = p.h_q / p.h_k;
-  int hpw = 256 / BQ;  // up to 256 query rows (four waves) per workgroup
+  int hpw = 256 / BQ;  // up to 256 query rows per workgroup
   while (hpw > 1 && G % hpw != 0) hpw >>= 1;
   const int n_hgroups = p.h_q / hpw;
   const int waves = hpw * C::WPH;
@@ -720,6 +720,12 @@ hipError_t launch_dq(const cowa_params& p, const SchedView& sv, const void* q, c
 int bwd_main_max_qblocks(int d, int tk) {
   if (d == 128) return tk == 128 ? BwdCfg<128, 128>::max_qblocks() : BwdCfg<128, 64>::max_qblocks();
   return tk == 128 ? BwdCfg<64, 128>::max_qblocks() : BwdCfg<64, 64>::max_qblocks();
+}
+
+int bwd_dq_max_kblocks(int d, int tk) {
+  // the LDS of the dQ pass: two K/V blocks, then one row's block list
+  if (d == 128) return tk == 128 ? DqCfg<128, 128, 128>::max_kblocks() : DqCfg<128, 128, 64>::max_kblocks();
+  return tk == 128 ? DqCfg<64, 128, 128>::max_kblocks() : DqCfg<64, 128, 64>::max_kblocks();
 }
 
 bool bwd_bf16_supported(int d, int tq, int tk) {

@@ -39,6 +39,8 @@ bool fwd_bf16_supported(int head_dim, int tile_q, int tile_k);
 bool bwd_bf16_supported(int head_dim, int tile_q, int tile_k);
 // the dK/dV pass keeps one column's block list in LDS: at most this many query blocks
 int bwd_main_max_qblocks(int head_dim, int tile_k);
+// the dQ pass keeps one row's block list in LDS: at most this many key blocks
+int bwd_dq_max_kblocks(int head_dim, int tile_k);
 
 hipError_t launch_fwd_bf16(const cowa_params& p, const SchedView& sv, const void* q, const void* k,
                            const void* v, void* o, float* lse, hipStream_t stream);

@@ -207,3 +207,24 @@ def test_decode_visible_keys_match_oracle():
     assert abi.cowa_decode_visible_keys(d, lens) == ref
     d = cowa.make_decode_params(64, 32, 8, 128, 131072, 128, 4096)
     assert abi.cowa_decode_visible_keys(d, [131072] * 64) == 64 * 8 * 20080
+
+
+@pytest.mark.parametrize("n_q,n_k,ok", [(16000 * 128, 16000 * 128, False), (8192 * 128, 8192 * 128, True),
+                                        (8192 * 128 + 1, 8192 * 128 + 1, False)])
+def test_bwd_shape_limits_on_host(n_q, n_k, ok):
+    """The backward passes keep one schedule row / column of block entries in
+    LDS; shapes beyond those limits are rejected before any launch (checked on
+    the host, so the error comes back without a device)."""
+    lib = _lib()
+    p = cowa.make_params(1, n_q, n_k, 4, 1, 128, 128, 4096, 128, 128)
+    need = ctypes.c_size_t()
+    st = lib.cowa_bwd_workspace_size(ctypes.byref(p), ctypes.byref(need))
+    assert st == abi.COWA_OK
+    s = abi.cowa_schedule_t()
+    vp = ctypes.c_void_p
+    st = lib.cowa_bwd_main(ctypes.byref(p), ctypes.byref(s), *[vp(1 << 24)] * 7, vp(1 << 24), need, vp(0))
+    if ok:
+        assert st != abi.COWA_ERR_UNSUPPORTED
+    else:
+        assert st == abi.COWA_ERR_UNSUPPORTED
+        assert b"blocks" in lib.cowa_last_error()
