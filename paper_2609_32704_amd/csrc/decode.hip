@@ -22,7 +22,6 @@ namespace {
 constexpr int kDefaultSplitKeys = 512;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
-constexpr int kUnroll = 4;  // key steps in flight per lane group
 
 struct DecArgs {
   const __bf16* q;
@@ -46,10 +45,32 @@ __device__ inline void bf16x8_to_f32(const uint4& w, float* f) {
   }
 }
 
+// Sum over the DC lanes of each lane group (DC = 8 or 16 consecutive lanes,
+// inside one 16-lane DPP row), the result in every lane of the group:
+// quad butterflies, then mirrors within 8 and within 16 lanes.
+template <int DC>
+__device__ inline float group_sum(float x) {
+  auto dpp = [](float v, int ctrl) -> float {
+    switch (ctrl) {  // the DPP control must be a constant
+      case 0xB1: return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+      case 0x4E: return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x4E, 0xF, 0xF, false));
+      case 0x141: return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x141, 0xF, 0xF, false));
+      default: return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x140, 0xF, 0xF, false));
+    }
+  };
+  x += dpp(x, 0xB1);   // quad_perm [1,0,3,2]: lane ^ 1
+  x += dpp(x, 0x4E);   // quad_perm [2,3,0,1]: lane ^ 2
+  x += dpp(x, 0x141);  // row_half_mirror: lane i <-> 7 - i within 8 lanes (the other quad)
+  if constexpr (DC == 16) x += dpp(x, 0x140);  // row_mirror: lane i <-> 15 - i (the other half row)
+  return x;
+}
+
 template <int D, int G>
 __global__ void __launch_bounds__(256) decode_split(DecArgs a) {
-  constexpr int DC = D / 8;     // lanes per cache row
-  constexpr int KG = 64 / DC;   // rows per wave step
+  constexpr int DC = D / 8;               // lanes per cache row (16-byte chunks)
+  constexpr int KG = 64 / DC;             // rows per wave load instruction
+  constexpr int STEP = 4 * KG;            // keys per workgroup step (4 waves)
+  constexpr int U = G >= 8 ? 4 : 8;       // steps in flight per iteration
   __shared__ float sm_m[4][G], sm_l[4][G];
   __shared__ float sm_o[4][G][D];
 
@@ -71,14 +92,12 @@ __global__ void __launch_bounds__(256) decode_split(DecArgs a) {
   const int32_t v0 = s * a.split_keys;
   const int32_t v1 = min(v0 + a.split_keys, total);
 
-  // query slices of the G QO heads, pre-scaled by scale * log2(e)
-  float qv[G][8];
+  // query chunk of each QO head as packed bf16 pairs (dot products in fp32)
+  uint32_t qp[G][4];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
     const uint4 w = *reinterpret_cast<const uint4*>(a.q + ((int64_t)b * a.h_q + hk * G + g) * D + dc * 8);
-    bf16x8_to_f32(w, qv[g]);
-#pragma unroll
-    for (int t = 0; t < 8; ++t) qv[g][t] *= a.c;
+    qp[g][0] = w.x; qp[g][1] = w.y; qp[g][2] = w.z; qp[g][3] = w.w;
   }
   float m[G], l[G], acc[G][8];
 #pragma unroll
@@ -92,58 +111,68 @@ __global__ void __launch_bounds__(256) decode_split(DecArgs a) {
   const int64_t head_off = ((int64_t)b * a.h_k + hk) * a.n_max * D;
   const __bf16* kbase = a.kc + head_off + dc * 8;
   const __bf16* vbase = a.vc + head_off + dc * 8;
-  constexpr int BLOCK_STEP = 4 * KG;  // rows per workgroup step
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-  for (int32_t vb = v0; vb < v1; vb += BLOCK_STEP * kUnroll) {
-    uint4 kr[kUnroll], vr[kUnroll];
-    bool ok[kUnroll];
+  // the split's visible positions [v0, v1) cover at most three contiguous key
+  // runs; each run is streamed as a contiguous key range
+  int32_t off = 0;
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int32_t vi = vb + u * BLOCK_STEP + wave * KG + kg;
-      ok[u] = vi < v1;
-      kr[u] = make_uint4(0, 0, 0, 0);
-      vr[u] = make_uint4(0, 0, 0, 0);
-      if (ok[u]) {
-        const int64_t key = run_key(runs, vi);
-        kr[u] = *reinterpret_cast<const uint4*>(kbase + key * D);
-        vr[u] = *reinterpret_cast<const uint4*>(vbase + key * D);
+  for (int r = 0; r < 3; ++r) {  // unrolled: the run arrays stay in registers
+    if (r >= runs.n) break;
+    const int32_t len = runs.b[r] - runs.a[r] + 1;
+    const int32_t lo = max(v0, off), hi = min(v1, off + len);
+    off += len;
+    if (lo >= hi) continue;
+    const int32_t k_lo = runs.a[r] + (lo - off + len), k_hi = runs.a[r] + (hi - off + len);  // keys [k_lo, k_hi)
+    for (int32_t kb = k_lo; kb < k_hi; kb += STEP * U) {
+      uint4 kr[U], vr[U];
+      bool ok[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int32_t key = kb + u * STEP + wave * KG + kg;
+        ok[u] = key < k_hi;
+        const int64_t kc = ok[u] ? key : k_hi - 1;
+        kr[u] = *reinterpret_cast<const uint4*>(kbase + kc * D);
+        vr[u] = *reinterpret_cast<const uint4*>(vbase + kc * D);
       }
-    }
-    float sc[G][kUnroll];
+      float sc[U][G];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      float kf[8];
-      bf16x8_to_f32(kr[u], kf);
+      for (int u = 0; u < U; ++u) {
+        const uint32_t kw[4] = {kr[u].x, kr[u].y, kr[u].z, kr[u].w};
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          float part = 0.f;
+#pragma unroll
+          for (int t = 0; t < 4; ++t)
+            part = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, qp[g][t]),
+                                                   __builtin_bit_cast(bf16x2, kw[t]), part, false);
+          part = group_sum<DC>(part);
+          sc[u][g] = ok[u] ? part * a.c : -INFINITY;
+        }
+      }
 #pragma unroll
       for (int g = 0; g < G; ++g) {
-        float part = 0.f;
+        float mx = sc[0][g];
 #pragma unroll
-        for (int t = 0; t < 8; ++t) part = fmaf(qv[g][t], kf[t], part);
+        for (int u = 1; u < U; ++u) mx = fmaxf(mx, sc[u][g]);
+        const float m_new = fmaxf(m[g], mx);
+        const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        const float alpha = __builtin_amdgcn_exp2f(m[g] - m_use);
+        l[g] *= alpha;
 #pragma unroll
-        for (int off = 1; off < DC; off <<= 1) part += __shfl_xor(part, off);
-        sc[g][u] = ok[u] ? part : -INFINITY;
-      }
-    }
+        for (int t = 0; t < 8; ++t) acc[g][t] *= alpha;
+        m[g] = m_new;
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      float mx = sc[g][0];
+        for (int u = 0; u < U; ++u) {
+          const float p = __builtin_amdgcn_exp2f(sc[u][g] - m_use);
+          l[g] += p;
+          const uint32_t vw[4] = {vr[u].x, vr[u].y, vr[u].z, vr[u].w};
 #pragma unroll
-      for (int u = 1; u < kUnroll; ++u) mx = fmaxf(mx, sc[g][u]);
-      const float m_new = fmaxf(m[g], mx);
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = __builtin_amdgcn_exp2f(m[g] - m_use);
-      l[g] *= alpha;
-#pragma unroll
-      for (int t = 0; t < 8; ++t) acc[g][t] *= alpha;
-      m[g] = m_new;
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const float p = __builtin_amdgcn_exp2f(sc[g][u] - m_use);
-        l[g] += p;
-        float vf[8];
-        bf16x8_to_f32(vr[u], vf);
-#pragma unroll
-        for (int t = 0; t < 8; ++t) acc[g][t] = fmaf(p, vf[t], acc[g][t]);
+          for (int t = 0; t < 4; ++t) {
+            acc[g][2 * t] = fmaf(p, __uint_as_float(vw[t] << 16), acc[g][2 * t]);
+            acc[g][2 * t + 1] = fmaf(p, __uint_as_float(vw[t] & 0xffff0000u), acc[g][2 * t + 1]);
+          }
+        }
       }
     }
   }
