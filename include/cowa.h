@@ -104,7 +104,8 @@ typedef struct {
   int32_t n_max;          /* KV-cache capacity (row stride) per sequence and head */
   int32_t w_sink, w_near; /* >= 0 */
   int32_t h_k_total, h_k_offset;
-  int32_t split_keys;     /* visible keys per split program; 0 = library default */
+  int32_t split_keys;     /* visible keys per split program (a multiple of 64); 0 = library
+                             default: ~1024 programs in total, each >= 256 keys */
   float softmax_scale;    /* > 0 */
   int32_t dtype;          /* COWA_BF16 */
 } cowa_decode_params;

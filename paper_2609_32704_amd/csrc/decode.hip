@@ -19,7 +19,8 @@
 namespace cowa {
 namespace {
 
-constexpr int kDefaultSplitKeys = 512;
+constexpr int kDefaultSplitKeys = 256;   // smallest default split
+constexpr int64_t kTargetPrograms = 1024;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -276,8 +277,19 @@ hipError_t launch_dg(const DecArgs& a, hipStream_t stream) {
 
 }  // namespace
 
+// Default split size: about kTargetPrograms split programs in total (four
+// per compute unit of an MI355X), each streaming one contiguous share of a
+// (sequence, KV head)'s visible keys; at least kDefaultSplitKeys keys, a
+// multiple of 256.  Fewer, longer splits amortise each program's start-up
+// (the first loads' latency, the key-run set-up) and its merge.
 int32_t decode_split_keys(const cowa_decode_params& p) {
-  return p.split_keys > 0 ? p.split_keys : kDefaultSplitKeys;
+  if (p.split_keys > 0) return p.split_keys;
+  const int64_t per = (int64_t)p.batch * p.h_k;
+  const int64_t splits = per >= kTargetPrograms ? 1 : (kTargetPrograms + per - 1) / per;
+  const int64_t v = max_visible(p);
+  int64_t sk = (v + splits - 1) / splits;
+  sk = (sk + 255) / 256 * 256;
+  return (int32_t)(sk < kDefaultSplitKeys ? kDefaultSplitKeys : sk);
 }
 
 int32_t decode_num_splits(const cowa_decode_params& p) {
