@@ -26,10 +26,11 @@ FLAGS = [
 ]
 
 
-# Per-file options.  The backward kernels are register-allocated with MFMA
-# results in VGPRs (their K/V operand fragments are pinned to AGPRs instead).
+# Per-file options.  The bf16 matrix kernels are register-allocated with MFMA
+# results in VGPRs (their reused operand fragments are pinned to AGPRs instead).
 FILE_FLAGS = {
     "bwd_bf16.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "fwd_bf16.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 
 

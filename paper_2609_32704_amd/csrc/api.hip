@@ -235,6 +235,9 @@ cowa_status cowa_fwd(const cowa_params* p, const cowa_schedule_t* s, const void*
     return fail(COWA_ERR_UNSUPPORTED, "too many query blocks for one launch");
   if (p->dtype == COWA_BF16 && !cowa::fwd_bf16_supported(p->head_dim, p->tile_q, p->tile_k))
     return fail(COWA_ERR_UNSUPPORTED, "bf16 forward is built for tile_q in {64,128}, tile_k in {32,64,128}");
+  if (p->dtype == COWA_BF16 && s->n_kt > cowa::fwd_bf16_max_kblocks(p->head_dim, p->tile_k))
+    return fail(COWA_ERR_UNSUPPORTED, "bf16 forward supports at most %d key blocks (got %d)",
+                cowa::fwd_bf16_max_kblocks(p->head_dim, p->tile_k), s->n_kt);
   COWA_TRY(check_device());
   const cowa::SchedView sv = cowa::sched_view(s);
   hipStream_t st = static_cast<hipStream_t>(stream);

@@ -30,19 +30,29 @@
 namespace cowa {
 namespace {
 
-template <int D, int BQ, int BK, int NQW>
-__global__ void __launch_bounds__(512) fwd_bf16_kernel(cowa_params p, SchedView sv, int hpw, int n_hgroups,
+template <int D, int BQ, int BK>
+struct FwdCfg {
+  static constexpr int NQW = 64;          // query rows per wave
+  static constexpr int NTQ = NQW / 16;    // query tiles per wave (columns of S^T)
+  static constexpr int KSD = D / 32;      // k-steps over d
+  static constexpr int MTD = D / 16;      // d tiles of O^T
+  static constexpr int NCH = BK / 32;     // 32-key chunks per block (one k-step of O^T += V^T P^T)
+  static constexpr int WPH = BQ / NQW;    // waves per QO head
+  using T = SwzTile<D, BK>;
+  static constexpr int MAIN_BYTES = 4 * T::BYTES;  // K, V of two blocks; then the row's entry lists
+  static constexpr int LDS_MAX = 160 * 1024;
+  static int lds_bytes(int n_kt) { return MAIN_BYTES + 4 * n_kt + 16; }  // + a vote word
+  static int max_kblocks() { return (LDS_MAX - MAIN_BYTES - 16) / 4; }
+};
+
+template <int D, int BQ, int BK>
+__global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView sv, int hpw, int n_hgroups,
                                                        const __bf16* __restrict__ q, const __bf16* __restrict__ k,
                                                        const __bf16* __restrict__ v, __bf16* __restrict__ o,
                                                        float* __restrict__ lse) {
-  using T = SwzTile<D, BK>;
-  constexpr int NTQ = NQW / 16;           // query tiles per wave
-  constexpr int BKC = BK > 64 ? 64 : BK;   // keys per softmax step (a KV block is 1 or 2 steps)
-  constexpr int MTK = BKC / 16;           // key tiles of S^T
-  constexpr int KSD = D / 32;             // k-steps over d
-  constexpr int MTD = D / 16;             // d tiles of O^T
-  constexpr int KSK = BKC / 32;           // k-steps over keys
-  constexpr int WAVES_PER_HEAD = BQ / NQW;
+  using C = FwdCfg<D, BQ, BK>;
+  using T = typename C::T;
+  constexpr int NTQ = C::NTQ, KSD = C::KSD, MTD = C::MTD, NCH = C::NCH;
   extern __shared__ __align__(1024) unsigned char smem[];
 
   const int nw = blockDim.x >> 6;
@@ -58,174 +68,271 @@ __global__ void __launch_bounds__(512) fwd_bf16_kernel(cowa_params p, SchedView 
 
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int lr = lane & 15, lg = lane >> 4;
-  const int h = h0 + wave / WAVES_PER_HEAD;
-  const int64_t q_first = (int64_t)i * BQ + (wave % WAVES_PER_HEAD) * NQW;
+  const int h = h0 + wave / C::WPH;
+  const int q_first = i * BQ + (wave % C::WPH) * C::NQW;
   const Geo32 g = geo32(make_geo(p.n_q, p.n_k, p.w_sink, p.w_near, BQ, BK, p.h_k_offset + hk, p.h_k_total));
 
   const __bf16* kbase = k + ((int64_t)b * p.h_k + hk) * p.n_k * D;
   const __bf16* vbase = v + ((int64_t)b * p.h_k + hk) * p.n_k * D;
+  const uint32_t smem_base = lds_addr(smem);
+
+  // the row's entries, split into full (from the front) and partial (from the back) lists
   const int r = hk * sv.n_qt + i;
   const int e0 = sv.fwd_row_ptr[r], e1 = sv.fwd_row_ptr[r + 1];
-
-  // buffer s: K at smem + 2 s BYTES, V right after it
-  if (e0 < e1) {
-    const int64_t kf = (int64_t)(sv.fwd_ent[e0] >> 1) * BK;
-    load_tile_asm_nw<D, BK>(kbase, (int)kf, p.n_k, lds_addr(smem), wave, nw, lane);
-    load_tile_asm_nw<D, BK>(vbase, (int)kf, p.n_k, lds_addr(smem) + T::BYTES, wave, nw, lane);
+  const int n_ent = e1 - e0;
+  const int cap = sv.n_kt;
+  uint32_t* list = reinterpret_cast<uint32_t*>(smem + C::MAIN_BYTES);
+  int n_full = 0;
+  for (int c0 = 0; c0 < n_ent; c0 += 64) {
+    const bool in = c0 + lane < n_ent;
+    const uint32_t ent = in ? sv.fwd_ent[e0 + c0 + lane] : 0u;
+    const uint64_t full = __ballot(in && !(ent & 1u));
+    const uint64_t part = __ballot(in && (ent & 1u));
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    if (wave == 0 && in) {
+      if (ent & 1u)
+        list[cap - 1 - (c0 - n_full + __popcll(part & below))] = ent;
+      else
+        list[n_full + __popcll(full & below)] = ent;
+    }
+    n_full += __popcll(full);
   }
+  auto entry_at = [&](int t) -> uint32_t {
+    const int tt = t < n_ent ? t : n_ent - 1;
+    const int idx = tt < n_full ? tt : cap - 1 - (tt - n_full);
+    return __builtin_amdgcn_readfirstlane(list[idx]);
+  };
+  auto stage = [&](uint32_t ent, int buf) {
+    const int kf = (int)(ent >> 1) * BK;
+    load_tile_asm_nw<D, BK>(kbase, kf, p.n_k, smem_base + buf * 2 * T::BYTES, wave, nw, lane);
+    load_tile_asm_nw<D, BK>(vbase, kf, p.n_k, smem_base + buf * 2 * T::BYTES + T::BYTES, wave, nw, lane);
+  };
+  __syncthreads();  // the lists are in LDS
 
-  // Q^T fragments (B operand): query column nt*16 + lr, d = ks*32 + 8*lg + 0..7
+  // Q^T fragments (B operands): query column nt*16 + lr, d = ks*32 + 8*lg + 0..7
+  const int64_t row_base = ((int64_t)b * p.h_q + h) * p.n_q;
   bf16x8 qf[NTQ][KSD];
 #pragma unroll
   for (int nt = 0; nt < NTQ; ++nt) {
-    const int64_t qp = q_first + nt * 16 + lr;
+    const int qp = q_first + nt * 16 + lr;
     const bool ok = qp < p.n_q;
-    const __bf16* qrow = q + (((int64_t)b * p.h_q + h) * p.n_q + (ok ? qp : 0)) * D;
+    const __bf16* qrow = q + (row_base + (ok ? qp : 0)) * D;
 #pragma unroll
     for (int ks = 0; ks < KSD; ++ks) {
-      bf16x8 val = *reinterpret_cast<const bf16x8*>(qrow + ks * 32 + 8 * lg);
+      const bf16x8 val = *reinterpret_cast<const bf16x8*>(qrow + ks * 32 + 8 * lg);
       qf[nt][ks] = ok ? val : bf16x8{};
     }
   }
-
-  f32x4 oacc[MTD][NTQ];
+  f32x4 oacc[MTD][NTQ];  // O^T: rows d, columns queries
 #pragma unroll
   for (int md = 0; md < MTD; ++md)
 #pragma unroll
     for (int nt = 0; nt < NTQ; ++nt) oacc[md][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run[NTQ], l_run[NTQ];
+  // The exponent offset m (base 2, per query column) is fixed once per row:
+  // the maximum over the first 32 keys of the row's first block.  P = exp2(s c - m)
+  // can then exceed 1, but O and l share the offset, so O / l and
+  // LSE = (m + log2 l) ln 2 are unaffected; no O rescaling is ever needed.  If a
+  // later score exceeds m by more than kLimit (P > 2^kLimit, where bf16 P and
+  // fp32 sums would approach their range), the workgroup runs the row again
+  // with m set to the row maximum found by the first pass.
+  constexpr float kLimit = 64.f;
+  float m_fix[NTQ], m_hi[NTQ], l_run[NTQ];  // m_hi: this lane's maximum raw score per column
 #pragma unroll
-  for (int nt = 0; nt < NTQ; ++nt) { m_run[nt] = -INFINITY; l_run[nt] = 0.f; }
+  for (int nt = 0; nt < NTQ; ++nt) {
+    m_fix[nt] = -INFINITY;
+    m_hi[nt] = -INFINITY;
+    l_run[nt] = 0.f;
+  }
   const float c = p.softmax_scale * kLog2e;
+  int offr[KSD], offt[MTD];
+#pragma unroll
+  for (int ks = 0; ks < KSD; ++ks) offr[ks] = row8_off<D>(lr, lg, ks);
+#pragma unroll
+  for (int md = 0; md < MTD; ++md) offt[md] = tr8_off<D>(lr, lg, md);
 
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
+  f32x4 sacc[2][NTQ];    // S^T of the chunk's two 16-key tiles: rows keys 4 lg + rr, column query 16 nt + lr
+  bf16x8 pb[2][NTQ];     // P^T of the current and the previous chunk as B operands
 
-  // schedule entries one and two blocks ahead are read early, so that no
-  // iteration waits on the load of the entry it prefetches
-  uint32_t ent_cur = e0 < e1 ? sv.fwd_ent[e0] : 0u;
-  uint32_t ent_nxt = e0 + 1 < e1 ? sv.fwd_ent[e0 + 1] : 0u;
-  for (int e = e0; e < e1; ++e) {
-    const int buf = (e - e0) & 1;
-    const uint32_t ent = ent_cur;
-    const int j = (int)(ent >> 1);
-    const bool partial = ent & 1u;
-    const int64_t k_first = (int64_t)j * BK;
-    if (e + 1 < e1) {  // prefetch the next block into the other buffer
-      const int64_t kf = (int64_t)(ent_nxt >> 1) * BK;
-      unsigned char* nb = smem + (buf ^ 1) * 2 * T::BYTES;
-      load_tile_asm_nw<D, BK>(kbase, (int)kf, p.n_k, lds_addr(nb), wave, nw, lane);
-      load_tile_asm_nw<D, BK>(vbase, (int)kf, p.n_k, lds_addr(nb) + T::BYTES, wave, nw, lane);
+  // softmax of a chunk (key0: its first key) into pb[sl]
+  auto softmax = [&](int sl, bool masked, int key0) __attribute__((always_inline)) {
+    if (masked) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int nt = 0; nt < NTQ; ++nt)
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr)
+            // an add that reads the accumulator: a plain masked store of -inf
+            // into an MFMA destination could be overtaken by the MFMA write
+            sacc[t][nt][rr] += legal32(g, q_first + nt * 16 + lr, key0 + t * 16 + 4 * lg + rr) ? 0.f : -INFINITY;
     }
-    ent_cur = ent_nxt;
-    ent_nxt = sv.fwd_ent[e + 2 < e1 ? e + 2 : e1 - 1];  // unconditional: no merge of wait states
+#pragma unroll
+    for (int nt = 0; nt < NTQ; ++nt) {
+      const float lm = fmaxf(fmaxf(fmaxf(sacc[0][nt][0], sacc[0][nt][1]), fmaxf(sacc[0][nt][2], sacc[0][nt][3])),
+                             fmaxf(fmaxf(sacc[1][nt][0], sacc[1][nt][1]), fmaxf(sacc[1][nt][2], sacc[1][nt][3])));
+      m_hi[nt] = fmaxf(m_hi[nt], lm);
+    }
+#pragma unroll
+    for (int nt = 0; nt < NTQ; ++nt) {
+      const float mu = m_fix[nt] == -INFINITY ? 0.f : m_fix[nt];
+      float ls = 0.f;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[t][nt][rr], c, -mu));
+          ls += pv;
+          pb[sl][nt][4 * t + rr] = (__bf16)pv;
+        }
+      l_run[nt] += ls;
+    }
+  };
+
+  // A block: for each chunk, 2 KSD groups of S^T (one K row fragment, NTQ
+  // MFMAs each), then MTD groups of O^T += V^T P^T for the previous chunk (one
+  // V^T fragment, NTQ MFMAs each) beside this chunk's softmax; a last MTD
+  // groups for the block's final chunk.  Fragments are read one group ahead.
+  constexpr int GPC = 2 * KSD + MTD, NGB = NCH * GPC + MTD;
+  auto load_g = [&](const unsigned char* Kt, const unsigned char* Vt, int gg, bf16x8& fa) __attribute__((always_inline)) {
+    if (gg < NCH * GPC) {
+      const int ch = gg / GPC, rr = gg % GPC;
+      if (rr < 2 * KSD) {
+        const int t = rr / KSD, ks = rr % KSD;
+        fa = ld_row8(Kt + offr[ks] + (ch * 32 + t * 16) * D * 2);
+      } else if (ch > 0) {
+        fa = ld_tr8(Vt + offt[rr - 2 * KSD] + (ch - 1) * 32 * D * 2, D * 2);
+      }
+    } else {
+      fa = ld_tr8(Vt + offt[gg - NCH * GPC] + (NCH - 1) * 32 * D * 2, D * 2);
+    }
+  };
+
+  auto block = [&](int t, bool masked) {
+    const int buf = t & 1;
+    const uint32_t ent = entry_at(t);
+    const int k_first = (int)(ent >> 1) * BK;
+    if (t + 1 < n_ent) stage(entry_at(t + 1), buf ^ 1);  // prefetch the next block
     const unsigned char* Kt = smem + buf * 2 * T::BYTES;
     const unsigned char* Vt = Kt + T::BYTES;
-
-#pragma unroll 1
-    for (int kc = 0; kc < BK; kc += BKC) {
-      // S^T = K_j Q^T : rows = keys (mt*16 + 4*lg + rr), column = query nt*16 + lr
-      f32x4 sacc[MTK][NTQ];
-  #pragma unroll
-      for (int mt = 0; mt < MTK; ++mt)
-  #pragma unroll
-        for (int nt = 0; nt < NTQ; ++nt) sacc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  #pragma unroll
-      for (int ks = 0; ks < KSD; ++ks)
-  #pragma unroll
-        for (int mt = 0; mt < MTK; ++mt) {
-          const int row = kc + mt * 16 + lr;
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(Kt + T::off(row, ks * 4 + lg));
-  #pragma unroll
+    bf16x8 fa[2];
+    load_g(Kt, Vt, 0, fa[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    static_for<NGB>([&](auto ic) {
+      constexpr int gg = decltype(ic)::value;
+      if constexpr (gg + 1 < NGB) load_g(Kt, Vt, gg + 1, fa[(gg + 1) & 1]);
+      const bf16x8& a = fa[gg & 1];
+      if constexpr (gg < NCH * GPC) {
+        constexpr int ch = gg / GPC, rr = gg % GPC;
+        if constexpr (rr < 2 * KSD) {
+          constexpr int tt = rr / KSD, ks = rr % KSD;
+#pragma unroll
           for (int nt = 0; nt < NTQ; ++nt)
-            sacc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[nt][ks], sacc[mt][nt], 0, 0, 0);
+            sacc[tt][nt] = mfma16(a, qf[nt][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sacc[tt][nt]);
+        } else {
+          constexpr int md = rr - 2 * KSD;
+          if constexpr (ch > 0) {
+#pragma unroll
+            for (int nt = 0; nt < NTQ; ++nt) oacc[md][nt] = mfma16(a, pb[(ch - 1) & 1][nt], oacc[md][nt]);
+          }
+          if constexpr (md == 0) softmax(ch & 1, masked, k_first + ch * 32);
         }
-
-      // online softmax per query column (raw-score units; c folded into the exponent)
-      if (partial) {
-  #pragma unroll
-        for (int nt = 0; nt < NTQ; ++nt) {
-          const int qp = (int)q_first + nt * 16 + lr;
-          const int k0 = (int)k_first + kc + 4 * lg;
-  #pragma unroll
-          for (int mt = 0; mt < MTK; ++mt)
-  #pragma unroll
-            for (int rr = 0; rr < 4; ++rr)
-              // an add that reads the accumulator: a plain masked store of -inf
-              // into an MFMA destination could be overtaken by the MFMA write
-              sacc[mt][nt][rr] += legal32(g, qp, k0 + mt * 16 + rr) ? 0.f : -INFINITY;
-        }
+      } else {
+        constexpr int md = gg - NCH * GPC;
+#pragma unroll
+        for (int nt = 0; nt < NTQ; ++nt) oacc[md][nt] = mfma16(a, pb[(NCH - 1) & 1][nt], oacc[md][nt]);
       }
-      float alpha[NTQ];
-      bool moved = false;
-  #pragma unroll
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    // register placement: O^T accumulators in VGPRs, Q^T fragments in AGPRs
+    // (read directly as B operands); these statements emit nothing
+#pragma unroll
+    for (int md = 0; md < MTD; ++md)
+#pragma unroll
+      for (int nt = 0; nt < NTQ; ++nt) asm volatile("" : "+v"(oacc[md][nt]));
+#pragma unroll
+    for (int nt = 0; nt < NTQ; ++nt)
+#pragma unroll
+      for (int ks = 0; ks < KSD; ++ks) asm volatile("" : "+a"(qf[nt][ks]));
+    __builtin_amdgcn_s_waitcnt(0);  // the next block has landed
+    __syncthreads();                 // ... for every wave, and this block is no longer read
+  };
+  for (int pass = 0; pass < 2; ++pass) {
+    if (n_ent > 0) stage(entry_at(0), 0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (pass == 0 && n_ent > 0) {
+      // offsets from the first 32 keys of the row's first block (in processing
+      // order: a full block when the row has one; its first key is legal for
+      // every query of a causal row either way)
+      const int key0 = (int)(entry_at(0) >> 1) * BK;
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int ks = 0; ks < KSD; ++ks) {
+          const bf16x8 a = ld_row8(smem + offr[ks] + tt * 16 * D * 2);
+#pragma unroll
+          for (int nt = 0; nt < NTQ; ++nt)
+            sacc[tt][nt] = mfma16(a, qf[nt][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sacc[tt][nt]);
+        }
+#pragma unroll
       for (int nt = 0; nt < NTQ; ++nt) {
-        float mx = -INFINITY;
-  #pragma unroll
-        for (int mt = 0; mt < MTK; ++mt)
-  #pragma unroll
-          for (int rr = 0; rr < 4; ++rr) mx = fmaxf(mx, sacc[mt][nt][rr]);
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run[nt], mx);
-        moved |= m_new > m_run[nt];
-        const float mc = m_new == -INFINITY ? 0.f : m_new * c;
-        alpha[nt] = __builtin_amdgcn_exp2f(m_run[nt] * c - mc);
-        m_run[nt] = m_new;
-        float lsum = 0.f;
-  #pragma unroll
-        for (int mt = 0; mt < MTK; ++mt)
-  #pragma unroll
+        float cm = -INFINITY;
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
           for (int rr = 0; rr < 4; ++rr) {
-            const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[mt][nt][rr], c, -mc));
-            sacc[mt][nt][rr] = pv;
-            lsum += pv;
+            const float sv2 = sacc[tt][nt][rr] + (legal32(g, q_first + nt * 16 + lr, key0 + tt * 16 + 4 * lg + rr) ? 0.f : -INFINITY);
+            cm = fmaxf(cm, sv2);
           }
-        l_run[nt] = l_run[nt] * alpha[nt] + lsum;
-      }
-      if (__any(moved)) {
-  #pragma unroll
-        for (int md = 0; md < MTD; ++md)
-  #pragma unroll
-          for (int nt = 0; nt < NTQ; ++nt) oacc[md][nt] *= alpha[nt];
-      }
-
-      // O^T += V_j^T P^T.  k-slot t of step ks is key 32ks + 4lg + t (t < 4) or
-      // 32ks + 16 + 4lg + (t - 4); the transposing read gives lane lr the column
-      // d = md*16 + lr of four keys, supplied by lanes 4*t + (lr / 4) of its group.
-  #pragma unroll
-      for (int ks = 0; ks < KSK; ++ks) {
-        bf16x8 pb[NTQ];
-  #pragma unroll
-        for (int nt = 0; nt < NTQ; ++nt)
-  #pragma unroll
-          for (int rr = 0; rr < 4; ++rr) {
-            pb[nt][rr] = (__bf16)sacc[2 * ks][nt][rr];
-            pb[nt][4 + rr] = (__bf16)sacc[2 * ks + 1][nt][rr];
-          }
-  #pragma unroll
-        for (int md = 0; md < MTD; ++md) {
-          const bf16x8 a = read_tr8<D, BK>(Vt, kc + ks * 32, md * 16, lr, lg);
-  #pragma unroll
-          for (int nt = 0; nt < NTQ; ++nt) oacc[md][nt] = mfma16(a, pb[nt], oacc[md][nt]);
-        }
+        cm = fmaxf(cm, __shfl_xor(cm, 16));
+        cm = fmaxf(cm, __shfl_xor(cm, 32));
+        m_fix[nt] = cm * c;  // -inf for a column without a legal key there
       }
     }
-
-    __builtin_amdgcn_s_waitcnt(0);  // the prefetch of block e+1 has landed
-    __syncthreads();                 // ... for every wave, and block e is no longer read
+    int t = 0;
+    for (; t < n_full; ++t) block(t, false);
+    for (; t < n_ent; ++t) block(t, true);
+    // did a score exceed its column's offset by more than kLimit?
+    bool far = false;
+#pragma unroll
+    for (int nt = 0; nt < NTQ; ++nt) {
+      float cm = m_hi[nt];
+      cm = fmaxf(cm, __shfl_xor(cm, 16));
+      cm = fmaxf(cm, __shfl_xor(cm, 32));
+      m_hi[nt] = cm * c;  // the column's maximum, in exponent units
+      // (a column whose offset is unset but which met legal keys later is run again too)
+      far |= m_hi[nt] != -INFINITY && (m_fix[nt] == -INFINITY || m_hi[nt] > m_fix[nt] + kLimit);
+    }
+    // workgroup vote through a word past the block lists
+    int* vote = reinterpret_cast<int*>(smem + C::MAIN_BYTES + 4 * cap);
+    if (tid == 0) *vote = 0;
+    __syncthreads();
+    if (far) *vote = 1;
+    __syncthreads();
+    const bool again = *vote != 0;
+    __syncthreads();
+    if (!again) break;
+    // run the row again with the row maxima as offsets (then P <= 1 everywhere)
+#pragma unroll
+    for (int nt = 0; nt < NTQ; ++nt) {
+      m_fix[nt] = m_hi[nt];
+      m_hi[nt] = -INFINITY;
+      l_run[nt] = 0.f;
+#pragma unroll
+      for (int md = 0; md < MTD; ++md) oacc[md][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
   }
 
-  // O = O / l; LSE = (m c + log2 l) ln 2
+  // O = O / l; LSE = (m + log2 l) ln 2 (m already in base-2 units)
 #pragma unroll
   for (int nt = 0; nt < NTQ; ++nt) {
     float lt = l_run[nt];
     lt += __shfl_xor(lt, 16);
     lt += __shfl_xor(lt, 32);
-    const int64_t qp = q_first + nt * 16 + lr;
+    const int qp = q_first + nt * 16 + lr;
     if (qp >= p.n_q) continue;
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
-    __bf16* orow = o + (((int64_t)b * p.h_q + h) * p.n_q + qp) * D;
+    __bf16* orow = o + (row_base + qp) * D;
 #pragma unroll
     for (int md = 0; md < MTD; ++md) {
       bf16x4 ov;
@@ -233,37 +340,43 @@ __global__ void __launch_bounds__(512) fwd_bf16_kernel(cowa_params p, SchedView 
       for (int rr = 0; rr < 4; ++rr) ov[rr] = (__bf16)(oacc[md][nt][rr] * inv);
       *reinterpret_cast<bf16x4*>(orow + md * 16 + 4 * lg) = ov;
     }
-    if (lg == 0)
-      lse[((int64_t)b * p.h_q + h) * p.n_q + qp] = lt > 0.f ? (m_run[nt] * c + __log2f(lt)) * kLn2 : -INFINITY;
+    if (lg == 0) lse[row_base + qp] = lt > 0.f ? (m_fix[nt] + __log2f(lt)) * kLn2 : -INFINITY;
   }
 }
 
-template <int D, int BQ, int BK, int NQW = 32>
+template <int D, int BQ, int BK>
 hipError_t launch_cfg(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
                       void* o, float* lse, hipStream_t stream) {
-  constexpr int LDS = 4 * SwzTile<D, BK>::BYTES;
-  static_assert(LDS <= 160 * 1024, "LDS budget");
-  auto kern = fwd_bf16_kernel<D, BQ, BK, NQW>;
+  using C = FwdCfg<D, BQ, BK>;
+  if (sv.n_kt > C::max_kblocks()) return hipErrorInvalidValue;
+  auto kern = fwd_bf16_kernel<D, BQ, BK>;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_MAX);
     if (err != hipSuccess) return err;
     attr_set = true;
   }
   const int G = p.h_q / p.h_k;
-  int hpw = 256 / BQ;  // QO heads per workgroup: up to 256 query rows
+  int hpw = 256 / BQ;  // QO heads per workgroup: up to 256 query rows (four waves)
   while (hpw > 1 && G % hpw != 0) hpw >>= 1;
   const int n_hgroups = p.h_q / hpw;
-  const int waves = hpw * (BQ / NQW);
+  const int waves = hpw * C::WPH;
   const unsigned blocks = (unsigned)sv.n_qt * n_hgroups * p.batch;
-  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * waves), LDS, stream, p, sv, hpw, n_hgroups,
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * waves), C::lds_bytes(sv.n_kt), stream, p, sv, hpw, n_hgroups,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), static_cast<const __bf16*>(v),
                      static_cast<__bf16*>(o), lse);
   return hipGetLastError();
 }
 
 }  // namespace
+
+int fwd_bf16_max_kblocks(int d, int tk) {
+  if (d == 128) return tk == 128 ? FwdCfg<128, 128, 128>::max_kblocks() : tk == 64 ? FwdCfg<128, 128, 64>::max_kblocks()
+                                                                                 : FwdCfg<128, 128, 32>::max_kblocks();
+  return tk == 128 ? FwdCfg<64, 128, 128>::max_kblocks() : tk == 64 ? FwdCfg<64, 128, 64>::max_kblocks()
+                                                                     : FwdCfg<64, 128, 32>::max_kblocks();
+}
 
 bool fwd_bf16_supported(int d, int tq, int tk) {
   return (d == 64 || d == 128) && (tq == 64 || tq == 128) && (tk == 32 || tk == 64 || tk == 128);

@@ -35,6 +35,8 @@ hipError_t launch_schedule(const cowa_schedule_t* s, hipStream_t stream);
 hipError_t launch_fwd_fp32(const cowa_params& p, const SchedView& sv, const float* q, const float* k,
                            const float* v, float* o, float* lse, hipStream_t stream);
 
+// the bf16 forward keeps one row's block list in LDS: at most this many key blocks
+int fwd_bf16_max_kblocks(int head_dim, int tile_k);
 bool fwd_bf16_supported(int head_dim, int tile_q, int tile_k);
 bool bwd_bf16_supported(int head_dim, int tile_q, int tile_k);
 // the dK/dV pass keeps one column's block list in LDS: at most this many query blocks
