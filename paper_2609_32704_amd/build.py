@@ -30,7 +30,6 @@ FLAGS = [
 # results in VGPRs (their reused operand fragments are pinned to AGPRs instead).
 FILE_FLAGS = {
     "bwd_bf16.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
-    "fwd_bf16.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 
 

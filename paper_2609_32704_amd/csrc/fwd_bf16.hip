@@ -36,15 +36,52 @@ struct FwdCfg {
   static constexpr int NTQ = NQW / 16;    // query tiles per wave (columns of S^T)
   static constexpr int KSD = D / 32;      // k-steps over d
   static constexpr int MTD = D / 16;      // d tiles of O^T
-  static constexpr int NCH = BK / 32;     // 32-key chunks per block (one k-step of O^T += V^T P^T)
+  static constexpr int NCH = BK / 32;     // 32-key chunks per block
+  static constexpr int NG = 2 * KSD + MTD;  // MFMA groups per chunk (NTQ MFMAs each)
   static constexpr int WPH = BQ / NQW;    // waves per QO head
   using T = SwzTile<D, BK>;
-  static constexpr int MAIN_BYTES = 4 * T::BYTES;  // K, V of two blocks; then the row's entry lists
+  static constexpr int MAIN_BYTES = 4 * T::BYTES;  // K and V of two blocks; then the row's entry lists
   static constexpr int LDS_MAX = 160 * 1024;
   static int lds_bytes(int n_kt) { return MAIN_BYTES + 4 * n_kt + 16; }  // + a vote word
   static int max_kblocks() { return (LDS_MAX - MAIN_BYTES - 16) / 4; }
+  static_assert(2 * KSD == MTD, "S and O groups alternate one to one");
 };
 
+// S^T = K Q^T products with the accumulator in VGPRs (read by the softmax on the
+// vector ALUs) while O^T accumulates in AGPRs: written as assembly because the
+// compiler gives all products of a kernel one accumulator register file.  The
+// compiler does not see these as matrix instructions and inserts no wait states
+// for them, so the schedule keeps their results at least four products away
+// from any reader (the softmax of a chunk runs one chunk after its S^T; the
+// k-steps of one tile are four products apart), and a block ends with explicit
+// wait states before its last S^T can be read.
+__device__ inline f32x4 mfma_v0(const bf16x8& a, const bf16x8& b) {
+  f32x4 d;
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=&v"(d) : "v"(a), "a"(b));
+  return d;
+}
+__device__ inline f32x4 mfma_v(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+  // accumulator input not tied to the output: the register allocator never
+  // needs a copy of a result that may still be in flight
+  f32x4 d;
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %3" : "=&v"(d) : "v"(a), "a"(b), "v"(c));
+  return d;
+}
+
+// max(a, b, c) in one instruction (fmaxf would first quiet each operand that
+// the compiler cannot prove canonical: the products above are opaque to it)
+__device__ inline float max3(float a, float b, float c) {
+  float d;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(d) : "v"(a), "v"(b), "v"(c));
+  return d;
+}
+
+#ifndef FWD_OPIN
+#define FWD_OPIN "a"
+#endif
+#ifndef FWD_QPIN
+#define FWD_QPIN "a"
+#endif
 template <int D, int BQ, int BK>
 __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView sv, int hpw, int n_hgroups,
                                                        const __bf16* __restrict__ q, const __bf16* __restrict__ k,
@@ -52,7 +89,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
                                                        float* __restrict__ lse) {
   using C = FwdCfg<D, BQ, BK>;
   using T = typename C::T;
-  constexpr int NTQ = C::NTQ, KSD = C::KSD, MTD = C::MTD, NCH = C::NCH;
+  constexpr int NTQ = C::NTQ, KSD = C::KSD, MTD = C::MTD, NCH = C::NCH, NG = C::NG;
   extern __shared__ __align__(1024) unsigned char smem[];
 
   const int nw = blockDim.x >> 6;
@@ -71,7 +108,6 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   const int h = h0 + wave / C::WPH;
   const int q_first = i * BQ + (wave % C::WPH) * C::NQW;
   const Geo32 g = geo32(make_geo(p.n_q, p.n_k, p.w_sink, p.w_near, BQ, BK, p.h_k_offset + hk, p.h_k_total));
-
   const __bf16* kbase = k + ((int64_t)b * p.h_k + hk) * p.n_k * D;
   const __bf16* vbase = v + ((int64_t)b * p.h_k + hk) * p.n_k * D;
   const uint32_t smem_base = lds_addr(smem);
@@ -102,10 +138,14 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
     const int idx = tt < n_full ? tt : cap - 1 - (tt - n_full);
     return __builtin_amdgcn_readfirstlane(list[idx]);
   };
-  auto stage = [&](uint32_t ent, int buf) {
-    const int kf = (int)(ent >> 1) * BK;
-    load_tile_asm_nw<D, BK>(kbase, kf, p.n_k, smem_base + buf * 2 * T::BYTES, wave, nw, lane);
-    load_tile_asm_nw<D, BK>(vbase, kf, p.n_k, smem_base + buf * 2 * T::BYTES + T::BYTES, wave, nw, lane);
+  // LDS: K of block t in K buffer t % 2, V of block t in V buffer t % 2
+  auto kbuf_off = [](int t) { return (t & 1) * 2 * T::BYTES; };
+  auto vbuf_off = [](int t) { return (t & 1) * 2 * T::BYTES + T::BYTES; };
+  auto stage_k = [&](int t) {
+    load_tile_asm_nw<D, BK>(kbase, (int)(entry_at(t) >> 1) * BK, p.n_k, smem_base + kbuf_off(t), wave, nw, lane);
+  };
+  auto stage_v = [&](int t) {
+    load_tile_asm_nw<D, BK>(vbase, (int)(entry_at(t) >> 1) * BK, p.n_k, smem_base + vbuf_off(t), wave, nw, lane);
   };
   __syncthreads();  // the lists are in LDS
 
@@ -124,10 +164,6 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
     }
   }
   f32x4 oacc[MTD][NTQ];  // O^T: rows d, columns queries
-#pragma unroll
-  for (int md = 0; md < MTD; ++md)
-#pragma unroll
-    for (int nt = 0; nt < NTQ; ++nt) oacc[md][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
   // The exponent offset m (base 2, per query column) is fixed once per row:
   // the maximum over the first 32 keys of the row's first block.  P = exp2(s c - m)
   // can then exceed 1, but O and l share the offset, so O / l and
@@ -136,13 +172,9 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   // fp32 sums would approach their range), the workgroup runs the row again
   // with m set to the row maximum found by the first pass.
   constexpr float kLimit = 64.f;
-  float m_fix[NTQ], m_hi[NTQ], l_run[NTQ];  // m_hi: this lane's maximum raw score per column
+  float m_fix[NTQ], m_hi[NTQ], l_run[NTQ], mu[NTQ];  // m_hi: this lane's maximum raw score per column
 #pragma unroll
-  for (int nt = 0; nt < NTQ; ++nt) {
-    m_fix[nt] = -INFINITY;
-    m_hi[nt] = -INFINITY;
-    l_run[nt] = 0.f;
-  }
+  for (int nt = 0; nt < NTQ; ++nt) m_fix[nt] = -INFINITY;
   const float c = p.softmax_scale * kLog2e;
   int offr[KSD], offt[MTD];
 #pragma unroll
@@ -150,114 +182,157 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
 #pragma unroll
   for (int md = 0; md < MTD; ++md) offt[md] = tr8_off<D>(lr, lg, md);
 
-  f32x4 sacc[2][NTQ];    // S^T of the chunk's two 16-key tiles: rows keys 4 lg + rr, column query 16 nt + lr
-  bf16x8 pb[2][NTQ];     // P^T of the current and the previous chunk as B operands
+  // Software pipeline over the row's 32-key chunks.  While the matrix cores
+  // compute S^T of chunk n (K fragments of the current block) and O^T += V^T P^T
+  // of a chunk one block back (V fragments of the previous block), the vector
+  // ALUs turn S^T of chunk n - 1 into P^T: the two streams are independent, so
+  // the exponentials of the softmax hide under the products.
+  f32x4 sacc[2][2][NTQ];  // S^T of two chunks ([chunk % 2][16-key tile][query tile])
+  bf16x8 pb[NCH][NTQ];    // P^T of the chunks of one block, as B operands
 
-  // softmax of a chunk (key0: its first key) into pb[sl]
-  auto softmax = [&](int sl, bool masked, int key0) __attribute__((always_inline)) {
-    if (masked) {
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int nt = 0; nt < NTQ; ++nt)
-#pragma unroll
-          for (int rr = 0; rr < 4; ++rr)
-            // an add that reads the accumulator: a plain masked store of -inf
-            // into an MFMA destination could be overtaken by the MFMA write
-            sacc[t][nt][rr] += legal32(g, q_first + nt * 16 + lr, key0 + t * 16 + 4 * lg + rr) ? 0.f : -INFINITY;
-    }
-#pragma unroll
-    for (int nt = 0; nt < NTQ; ++nt) {
-      const float lm = fmaxf(fmaxf(fmaxf(sacc[0][nt][0], sacc[0][nt][1]), fmaxf(sacc[0][nt][2], sacc[0][nt][3])),
-                             fmaxf(fmaxf(sacc[1][nt][0], sacc[1][nt][1]), fmaxf(sacc[1][nt][2], sacc[1][nt][3])));
-      m_hi[nt] = fmaxf(m_hi[nt], lm);
-    }
-#pragma unroll
-    for (int nt = 0; nt < NTQ; ++nt) {
-      const float mu = m_fix[nt] == -INFINITY ? 0.f : m_fix[nt];
-      float ls = 0.f;
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[t][nt][rr], c, -mu));
-          ls += pv;
-          pb[sl][nt][4 * t + rr] = (__bf16)pv;
-        }
-      l_run[nt] += ls;
+  // The softmax of one chunk is split into 32 element steps (element e: query
+  // tile e / 8, key tile (e / 4) % 2, row e % 4), spread evenly over NS slots
+  // of one MFMA each: first exponent, then sum, running maximum and packing.
+  float pv[32];  // exponentials in flight between the two halves of an element step
+  auto soft_a = [&](auto ec, auto rpc, bool masked, int key0) __attribute__((always_inline)) {
+    constexpr int e = decltype(ec)::value, rp = decltype(rpc)::value;
+    constexpr int nt = e / 8, tt = (e / 4) % 2, rr = e % 4;
+    if (masked)
+      sacc[rp][tt][nt][rr] += legal32(g, q_first + nt * 16 + lr, key0 + tt * 16 + 4 * lg + rr) ? 0.f : -INFINITY;
+    pv[e] = __builtin_amdgcn_exp2f(fmaf(sacc[rp][tt][nt][rr], c, -mu[nt]));
+  };
+  auto soft_b = [&](auto ec, auto rpc, auto psc) __attribute__((always_inline)) {
+    constexpr int e = decltype(ec)::value, rp = decltype(rpc)::value, ps = decltype(psc)::value;
+    constexpr int nt = e / 8, tt = (e / 4) % 2, rr = e % 4;
+    l_run[nt] += pv[e];
+    if constexpr (rr & 1) {
+      m_hi[nt] = max3(m_hi[nt], sacc[rp][tt][nt][rr - 1], sacc[rp][tt][nt][rr]);
+      pb[ps][nt][4 * tt + rr - 1] = (__bf16)pv[e - 1];
+      pb[ps][nt][4 * tt + rr] = (__bf16)pv[e];
     }
   };
-
-  // A block: for each chunk, 2 KSD groups of S^T (one K row fragment, NTQ
-  // MFMAs each), then MTD groups of O^T += V^T P^T for the previous chunk (one
-  // V^T fragment, NTQ MFMAs each) beside this chunk's softmax; a last MTD
-  // groups for the block's final chunk.  Fragments are read one group ahead.
-  constexpr int GPC = 2 * KSD + MTD, NGB = NCH * GPC + MTD;
-  auto load_g = [&](const unsigned char* Kt, const unsigned char* Vt, int gg, bf16x8& fa) __attribute__((always_inline)) {
-    if (gg < NCH * GPC) {
-      const int ch = gg / GPC, rr = gg % GPC;
-      if (rr < 2 * KSD) {
-        const int t = rr / KSD, ks = rr % KSD;
-        fa = ld_row8(Kt + offr[ks] + (ch * 32 + t * 16) * D * 2);
-      } else if (ch > 0) {
-        fa = ld_tr8(Vt + offt[rr - 2 * KSD] + (ch - 1) * 32 * D * 2, D * 2);
-      }
-    } else {
-      fa = ld_tr8(Vt + offt[gg - NCH * GPC] + (NCH - 1) * 32 * D * 2, D * 2);
-    }
-  };
-
-  auto block = [&](int t, bool masked) {
-    const int buf = t & 1;
-    const uint32_t ent = entry_at(t);
-    const int k_first = (int)(ent >> 1) * BK;
-    if (t + 1 < n_ent) stage(entry_at(t + 1), buf ^ 1);  // prefetch the next block
-    const unsigned char* Kt = smem + buf * 2 * T::BYTES;
-    const unsigned char* Vt = Kt + T::BYTES;
-    bf16x8 fa[2];
-    load_g(Kt, Vt, 0, fa[0]);
-    __builtin_amdgcn_sched_barrier(0);
-    static_for<NGB>([&](auto ic) {
-      constexpr int gg = decltype(ic)::value;
-      if constexpr (gg + 1 < NGB) load_g(Kt, Vt, gg + 1, fa[(gg + 1) & 1]);
-      const bf16x8& a = fa[gg & 1];
-      if constexpr (gg < NCH * GPC) {
-        constexpr int ch = gg / GPC, rr = gg % GPC;
-        if constexpr (rr < 2 * KSD) {
-          constexpr int tt = rr / KSD, ks = rr % KSD;
-#pragma unroll
-          for (int nt = 0; nt < NTQ; ++nt)
-            sacc[tt][nt] = mfma16(a, qf[nt][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sacc[tt][nt]);
-        } else {
-          constexpr int md = rr - 2 * KSD;
-          if constexpr (ch > 0) {
-#pragma unroll
-            for (int nt = 0; nt < NTQ; ++nt) oacc[md][nt] = mfma16(a, pb[(ch - 1) & 1][nt], oacc[md][nt]);
-          }
-          if constexpr (md == 0) softmax(ch & 1, masked, k_first + ch * 32);
-        }
-      } else {
-        constexpr int md = gg - NCH * GPC;
-#pragma unroll
-        for (int nt = 0; nt < NTQ; ++nt) oacc[md][nt] = mfma16(a, pb[(NCH - 1) & 1][nt], oacc[md][nt]);
-      }
-      __builtin_amdgcn_sched_barrier(0);
+  // the element steps of slot `slot` out of NS
+  auto soft_slot = [&](auto slotc, auto nsc, auto rpc, auto psc, bool masked, int key0) __attribute__((always_inline)) {
+    constexpr int slot = decltype(slotc)::value, NS = decltype(nsc)::value;
+    constexpr int LAG = NS >= 64 ? NS / 64 : 0;  // slots between the two halves of an element step
+    static_for<32>([&](auto ec) {
+      constexpr int e = decltype(ec)::value;
+      constexpr int sa = e * NS / 32;
+      if constexpr (sa == slot) soft_a(ec, rpc, masked, key0);
+      if constexpr (sa + LAG == slot) soft_b(ec, rpc, psc);
     });
-    // register placement: O^T accumulators in VGPRs, Q^T fragments in AGPRs
-    // (read directly as B operands); these statements emit nothing
+  };
+
+  // O^T += V^T P^T for chunk j of a block (V tile Vt) and S^T of chunk j (K tile
+  // Kt), group by group, fragments read PF groups ahead.  gi -> S group or O group.
+  constexpr int PF = 2;
+  int k_prev = 0;  // first key of the previous block
+  // One block of the pipeline.  FIRST: the row's first block (no previous block:
+  // no O^T products, no softmax before the first chunk).  MPREV / MCUR: the
+  // chunks softmaxed here from the previous / this block need the element mask.
+  auto step = [&](int t, auto firstc, auto mprevc, auto mcurc) __attribute__((always_inline)) {
+    constexpr bool FIRST = decltype(firstc)::value, MPREV = decltype(mprevc)::value, MCUR = decltype(mcurc)::value;
+    const int k_first = (int)(entry_at(t) >> 1) * BK;
+    if (t + 1 < n_ent) stage_k(t + 1);  // K buffer of block t - 1: free
+    stage_v(t);                         // V buffer of block t - 2: free
+    const unsigned char* Kt = smem + kbuf_off(t);
+    const unsigned char* Vp = smem + vbuf_off(t + 1);  // V of block t - 1
+    constexpr int NGS = NCH * NG;
+    bf16x8 fa[PF + 1];
+    auto load = [&](auto gc, bf16x8& dst) __attribute__((always_inline)) {
+      constexpr int GG = decltype(gc)::value, j = GG / NG, gi = GG % NG;
+      constexpr bool S = NCH >= 2 ? (gi % 2 == 0) : (gi < 2 * KSD);
+      constexpr int x = NCH >= 2 ? gi / 2 : (S ? gi : gi - 2 * KSD);
+      if constexpr (S) {
+        dst = ld_row8(Kt + offr[x % KSD] + (j * 32 + (x / KSD) * 16) * D * 2);
+      } else if constexpr (!FIRST) {
+        dst = ld_tr8(Vp + offt[x] + j * 32 * D * 2, D * 2);
+      }
+    };
+    static_for<PF>([&](auto ic) { load(ic, fa[decltype(ic)::value]); });
+    __builtin_amdgcn_sched_barrier(0);
+    static_for<NGS>([&](auto gc) {
+      constexpr int GG = decltype(gc)::value, j = GG / NG, gi = GG % NG;
+      constexpr bool S = NCH >= 2 ? (gi % 2 == 0) : (gi < 2 * KSD);
+      constexpr int x = NCH >= 2 ? gi / 2 : (S ? gi : gi - 2 * KSD);
+      if constexpr (GG + PF < NGS) load(std::integral_constant<int, GG + PF>{}, fa[(GG + PF) % (PF + 1)]);
+      const bf16x8& a = fa[GG % (PF + 1)];
+      // the softmax of the chunk before chunk j: chunk j - 1 of this block, or
+      // the last chunk of the previous block; spread over all groups, or for a
+      // one-chunk block over the S groups (its P^T is consumed within the block)
+      constexpr int NS = NCH >= 2 ? 4 * NG : 4 * 2 * KSD;
+      constexpr int ps = (j + NCH - 1) % NCH;
+      static_for<NTQ>([&](auto mc) {
+        constexpr int m = decltype(mc)::value;
+        if constexpr (S) {
+          constexpr int tt = x / KSD, ks = x % KSD;
+          if constexpr (ks == 0)
+            sacc[j & 1][tt][m] = mfma_v0(a, qf[m][ks]);
+          else
+            sacc[j & 1][tt][m] = mfma_v(a, qf[m][ks], sacc[j & 1][tt][m]);
+        } else if constexpr (!FIRST) {
+          oacc[x][m] = mfma16(a, pb[j][m], oacc[x][m]);
+        }
+        constexpr int slot = gi * NTQ + m;
+        if constexpr (!(FIRST && j == 0) && slot < NS) {
+          using SL = std::integral_constant<int, slot>;
+          using NSC = std::integral_constant<int, NS>;
+          using PS = std::integral_constant<int, ps>;
+          if constexpr (j == 0)
+            soft_slot(SL{}, NSC{}, std::integral_constant<int, 1>{}, PS{}, MPREV, k_prev + (NCH - 1) * 32);
+          else
+            soft_slot(SL{}, NSC{}, std::integral_constant<int, (j + 1) & 1>{}, PS{}, MCUR, k_first + (j - 1) * 32);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    });
+    // the last S^T products of the block may still be in flight (a first block
+    // has no O^T products after them): 16 wait states before anything reads them
+    asm volatile("s_nop 7\n\ts_nop 7");
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (NCH == 1) {
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int nt = 0; nt < NTQ; ++nt) sacc[1][tt][nt] = sacc[0][tt][nt];
+    }
+    // register placement: O^T accumulators and Q^T fragments in AGPRs (read
+    // directly by the matrix cores), S^T and P^T in VGPRs; these emit nothing
 #pragma unroll
     for (int md = 0; md < MTD; ++md)
 #pragma unroll
-      for (int nt = 0; nt < NTQ; ++nt) asm volatile("" : "+v"(oacc[md][nt]));
+      for (int nt = 0; nt < NTQ; ++nt) asm volatile("" : "+" FWD_OPIN(oacc[md][nt]));
 #pragma unroll
     for (int nt = 0; nt < NTQ; ++nt)
 #pragma unroll
-      for (int ks = 0; ks < KSD; ++ks) asm volatile("" : "+a"(qf[nt][ks]));
-    __builtin_amdgcn_s_waitcnt(0);  // the next block has landed
-    __syncthreads();                 // ... for every wave, and this block is no longer read
+      for (int ks = 0; ks < KSD; ++ks) asm volatile("" : "+" FWD_QPIN(qf[nt][ks]));
+    k_prev = k_first;
+    __builtin_amdgcn_s_waitcnt(0);  // block t + 1's K and block t's V have landed
+    __syncthreads();                 // ... for every wave, and the freed buffers are no longer read
   };
+  // after the last block: the softmax of its last chunk, then its O^T products
+  auto drain = [&](int t) __attribute__((always_inline)) {
+    using R1 = std::integral_constant<int, 1>;
+    static_for<32>([&](auto ec) { soft_a(ec, R1{}, true, k_prev + (NCH - 1) * 32); });
+    static_for<32>([&](auto ec) { soft_b(ec, R1{}, std::integral_constant<int, NCH - 1>{}); });
+    const unsigned char* Vt = smem + vbuf_off(t);
+    static_for<NCH * MTD>([&](auto gc) {
+      constexpr int GG = decltype(gc)::value, j = GG / MTD, md = GG % MTD;
+      const bf16x8 a = ld_tr8(Vt + offt[md] + j * 32 * D * 2, D * 2);
+#pragma unroll
+      for (int nt = 0; nt < NTQ; ++nt) oacc[md][nt] = mfma16(a, pb[j][nt], oacc[md][nt]);
+    });
+  };
+
   for (int pass = 0; pass < 2; ++pass) {
-    if (n_ent > 0) stage(entry_at(0), 0);
+#pragma unroll
+    for (int nt = 0; nt < NTQ; ++nt) {
+      m_hi[nt] = -INFINITY;
+      l_run[nt] = 0.f;
+#pragma unroll
+      for (int md = 0; md < MTD; ++md) oacc[md][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    if (n_ent > 0) stage_k(0);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (pass == 0 && n_ent > 0) {
@@ -272,7 +347,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
           const bf16x8 a = ld_row8(smem + offr[ks] + tt * 16 * D * 2);
 #pragma unroll
           for (int nt = 0; nt < NTQ; ++nt)
-            sacc[tt][nt] = mfma16(a, qf[nt][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sacc[tt][nt]);
+            sacc[0][tt][nt] = mfma16(a, qf[nt][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sacc[0][tt][nt]);
         }
 #pragma unroll
       for (int nt = 0; nt < NTQ; ++nt) {
@@ -281,7 +356,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
         for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
           for (int rr = 0; rr < 4; ++rr) {
-            const float sv2 = sacc[tt][nt][rr] + (legal32(g, q_first + nt * 16 + lr, key0 + tt * 16 + 4 * lg + rr) ? 0.f : -INFINITY);
+            const float sv2 = sacc[0][tt][nt][rr] + (legal32(g, q_first + nt * 16 + lr, key0 + tt * 16 + 4 * lg + rr) ? 0.f : -INFINITY);
             cm = fmaxf(cm, sv2);
           }
         cm = fmaxf(cm, __shfl_xor(cm, 16));
@@ -289,9 +364,23 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
         m_fix[nt] = cm * c;  // -inf for a column without a legal key there
       }
     }
+#pragma unroll
+    for (int nt = 0; nt < NTQ; ++nt) mu[nt] = m_fix[nt] == -INFINITY ? 0.f : m_fix[nt];
+    using TT = std::true_type;
+    using FF = std::false_type;
     int t = 0;
-    for (; t < n_full; ++t) block(t, false);
-    for (; t < n_ent; ++t) block(t, true);
+    if (n_full > 0) {
+      step(0, TT{}, FF{}, FF{});
+      for (t = 1; t < n_full; ++t) step(t, FF{}, FF{}, FF{});
+    }
+    if (t < n_ent) {
+      if (t == 0) {
+        step(0, TT{}, TT{}, TT{});
+        t = 1;
+      }
+      for (; t < n_ent; ++t) step(t, FF{}, TT{}, TT{});
+    }
+    if (n_ent > 0) drain(n_ent - 1);
     // did a score exceed its column's offset by more than kLimit?
     bool far = false;
 #pragma unroll
@@ -314,13 +403,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
     if (!again) break;
     // run the row again with the row maxima as offsets (then P <= 1 everywhere)
 #pragma unroll
-    for (int nt = 0; nt < NTQ; ++nt) {
-      m_fix[nt] = m_hi[nt];
-      m_hi[nt] = -INFINITY;
-      l_run[nt] = 0.f;
-#pragma unroll
-      for (int md = 0; md < MTD; ++md) oacc[md][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
+    for (int nt = 0; nt < NTQ; ++nt) m_fix[nt] = m_hi[nt];
   }
 
   // O = O / l; LSE = (m + log2 l) ln 2 (m already in base-2 units)
