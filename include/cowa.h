@@ -143,9 +143,11 @@ cowa_status cowa_schedule(const cowa_schedule_t* s, void* stream);
  * visible-key set.  q [B,H_q,N_q,d], k/v [B,H_k,N_k,d] -> o [B,H_q,N_q,d],
  * lse [B,H_q,N_q] float32.  `s` must have been sized for the same n_q, n_k,
  * h_k, windows, global head indexing and tiles, and built.  The bf16 path
+ * takes tile_q and tile_k in {64, 128} (COWA_ERR_UNSUPPORTED otherwise) and
  * keeps one schedule row in LDS: COWA_ERR_UNSUPPORTED (before any launch)
  * when ceil(N_k / tile_k) exceeds 8188 (head_dim 128, tile_k 128; 24572 for
- * tile_k 64 or head_dim 64 with tile_k 128), i.e. 1M key tokens at 128. */
+ * tile_k 64 or head_dim 64 with tile_k 128; 32764 for head_dim 64, tile_k
+ * 64), i.e. 1M key tokens at 128. */
 cowa_status cowa_fwd(const cowa_params* p, const cowa_schedule_t* s,
                      const void* q, const void* k, const void* v,
                      void* o, float* lse, void* stream);

@@ -30,42 +30,39 @@
 namespace cowa {
 namespace {
 
-template <int D, int BQ, int BK>
-struct FwdCfg {
-  static constexpr int NQW = 64;          // query rows per wave
-  static constexpr int NTQ = NQW / 16;    // query tiles per wave (columns of S^T)
-  static constexpr int KSD = D / 32;      // k-steps over d
-  static constexpr int MTD = D / 16;      // d tiles of O^T
-  static constexpr int NCH = BK / 32;     // 32-key chunks per block
-  static constexpr int NG = 2 * KSD + MTD;  // MFMA groups per chunk (NTQ MFMAs each)
-  static constexpr int WPH = BQ / NQW;    // waves per QO head
-  using T = SwzTile<D, BK>;
-  static constexpr int MAIN_BYTES = 4 * T::BYTES;  // K and V of two blocks; then the row's entry lists
-  static constexpr int LDS_MAX = 160 * 1024;
-  static int lds_bytes(int n_kt) { return MAIN_BYTES + 4 * n_kt + 16; }  // + a vote word
-  static int max_kblocks() { return (LDS_MAX - MAIN_BYTES - 16) / 4; }
-  static_assert(2 * KSD == MTD, "S and O groups alternate one to one");
-};
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 // S^T = K Q^T products with the accumulator in VGPRs (read by the softmax on the
 // vector ALUs) while O^T accumulates in AGPRs: written as assembly because the
 // compiler gives all products of a kernel one accumulator register file.  The
 // compiler does not see these as matrix instructions and inserts no wait states
-// for them, so the schedule keeps their results at least four products away
-// from any reader (the softmax of a chunk runs one chunk after its S^T; the
-// k-steps of one tile are four products apart), and a block ends with explicit
-// wait states before its last S^T can be read.
-__device__ inline f32x4 mfma_v0(const bf16x8& a, const bf16x8& b) {
-  f32x4 d;
-  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=&v"(d) : "v"(a), "a"(b));
+// for them, so the schedule keeps every reader of a result at least three
+// products behind it (the softmax of a chunk runs one chunk after its S^T; the
+// k-steps of one tile are three products apart, or separated by explicit wait
+// states), and a block ends with explicit wait states before its last S^T can
+// be read.  (A k-step chain accumulates in place; the schedule gives the
+// register allocator no reason to copy a result that may still be in flight,
+// which the kernel's assembly is checked for.)
+__device__ inline f32x16 mfma32_v0(const bf16x8& a, const bf16x8& b) {
+  f32x16 d;
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(d) : "v"(a), "a"(b));
   return d;
 }
-__device__ inline f32x4 mfma_v(const bf16x8& a, const bf16x8& b, const f32x4& c) {
-  // accumulator input not tied to the output: the register allocator never
-  // needs a copy of a result that may still be in flight
-  f32x4 d;
-  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %3" : "=&v"(d) : "v"(a), "a"(b), "v"(c));
+__device__ inline f32x16 mfma32_v(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  f32x16 d = c;
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(d) : "v"(a), "a"(b));
   return d;
+}
+__device__ inline f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+// wait states after the products above before their results are read; the
+// accumulators pass through the statement, so no reader is moved above it
+__device__ inline void mfma_settle(f32x16& a, f32x16& b) {
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(a), "+v"(b));
 }
 
 // max(a, b, c) in one instruction (fmaxf would first quiet each operand that
@@ -76,41 +73,105 @@ __device__ inline float max3(float a, float b, float c) {
   return d;
 }
 
-#ifndef FWD_OPIN
-#define FWD_OPIN "a"
-#endif
-#ifndef FWD_QPIN
-#define FWD_QPIN "a"
-#endif
+// Raw buffer resource over [base, base + bytes) (GFX9 layout, stride 0): loads
+// at offsets past `bytes` return zero instead of touching memory.
+__device__ inline i32x4 buffer_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)base;
+  return i32x4{(int)(uint32_t)a, (int)((a >> 32) & 0xffffu), (int)bytes, 0x00020000};
+}
+// 16 bytes per lane from a buffer straight into LDS: lane l lands at
+// lds_base + 16 l.  Issued as assembly and waited for explicitly, like dma16.
+__device__ inline void dma16_buf(uint32_t voff, i32x4 rsrc, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+               :
+               : "v"(voff), "s"(rsrc), "s"(lds_base)
+               : "memory", "m0");
+}
+
+// Workgroup -> (QO block i, head group, sequence).  Workgroups are handed to
+// the 8 XCDs round-robin by id, and each XCD has its own L2.  Work is cut into
+// clusters of 16 consecutive QO blocks x the head groups of one KV head: those
+// rows walk nearly the same K/V blocks, so an XCD running one cluster at a time
+// (32 workgroups with two head groups per KV head) serves most block copies
+// from its L2.  Clusters go out latest QO blocks first (the longest rows), and
+// the KV head of an XCD's cluster rotates from one range of QO blocks to the
+// next, so every XCD gets the same mix of short- and long-window heads.
+// Shapes that do not tile this way keep a plain order with chunks of 8
+// consecutive items per XCD.
+__device__ inline void fwd_work_item(int id, int n_qt, int n_hgroups, int batch, int h_k, int* i, int* hgi, int* b) {
+  constexpr int CQ = 16;
+  const int hg_per_hk = n_hgroups / h_k;
+  const int units = batch * h_k;                // (sequence, KV head) pairs
+  const int n_clusters = units * (n_qt / CQ);
+  const int cs = CQ * hg_per_hk;                // workgroups per cluster
+  if (n_qt % CQ == 0 && n_clusters % 8 == 0) {
+    const int xcd = id & 7, n = id >> 3;
+    const int c = (n / cs) * 8 + xcd, item = n % cs;
+    const int r = c / units;
+    const int u = (c % units + r) % units;
+    *b = u / h_k;
+    *hgi = (u % h_k) * hg_per_hk + item % hg_per_hk;
+    *i = n_qt - 1 - (r * CQ + item / hg_per_hk);
+    return;
+  }
+  const int total = n_qt * n_hgroups * batch;
+  const int work = xcd_remap(id, total);
+  const int per_i = n_hgroups * batch;
+  *i = n_qt - 1 - work / per_i;
+  const int rest = work % per_i;
+  *hgi = rest % n_hgroups;
+  *b = rest / n_hgroups;
+}
+
 template <int D, int BQ, int BK>
+struct FwdCfg {
+  static constexpr int NQW = 64;          // query rows per wave
+  static constexpr int NQT = NQW / 32;    // 32-query tiles per wave (columns of S^T)
+  static constexpr int KS = D / 16;       // k-steps over d of S^T = K Q^T
+  static constexpr int MD = D / 32;       // 32-row d tiles of O^T
+  static constexpr int NCH = BK / 32;     // 32-key chunks per block (2 or 4)
+  static constexpr int NG = KS + 2 * MD;  // product groups per chunk (NQT products each)
+  static constexpr int WPH = BQ / NQW;    // waves per QO head
+  using T = SwzTile<D, BK>;
+  static constexpr int MAIN_BYTES = 4 * T::BYTES;  // K and V of two blocks; then the row's entry lists
+  static constexpr int LDS_MAX = 160 * 1024;
+  static int lds_bytes(int n_kt) { return MAIN_BYTES + 4 * n_kt + 16; }  // + a vote word
+  static int max_kblocks() { return (LDS_MAX - MAIN_BYTES - 16) / 4; }
+  static_assert(KS == 2 * MD, "S and O groups alternate one to one");
+  static_assert(NCH == 2 || NCH == 4, "64- or 128-key blocks");
+};
+
+// FOUR: launched with four waves (the fast copy path; a compile-time choice
+// keeps the block step free of branches)
+template <int D, int BQ, int BK, bool FOUR>
 __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView sv, int hpw, int n_hgroups,
                                                        const __bf16* __restrict__ q, const __bf16* __restrict__ k,
                                                        const __bf16* __restrict__ v, __bf16* __restrict__ o,
                                                        float* __restrict__ lse) {
   using C = FwdCfg<D, BQ, BK>;
   using T = typename C::T;
-  constexpr int NTQ = C::NTQ, KSD = C::KSD, MTD = C::MTD, NCH = C::NCH, NG = C::NG;
+  constexpr int NQT = C::NQT, KS = C::KS, MD = C::MD, NCH = C::NCH, NG = C::NG;
   extern __shared__ __align__(1024) unsigned char smem[];
 
   const int nw = blockDim.x >> 6;
   const int G = p.h_q / p.h_k;
-  const int total = sv.n_qt * n_hgroups * p.batch;
-  const int work = xcd_remap(blockIdx.x, total);
-  const int per_i = n_hgroups * p.batch;
-  const int i = sv.n_qt - 1 - work / per_i;  // latest (longest) QO blocks first
-  const int rest = work % per_i;
-  const int hgi = rest % n_hgroups, b = rest / n_hgroups;
+  int i, hgi, b;
+  fwd_work_item(blockIdx.x, sv.n_qt, n_hgroups, p.batch, p.h_k, &i, &hgi, &b);
   const int hk = hgi / (G / hpw);
   const int h0 = hgi * hpw;  // first QO head of this workgroup (all in KV group hk)
 
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
-  const int lr = lane & 15, lg = lane >> 4;
-  const int h = h0 + wave / C::WPH;
+  const int l32 = lane & 31, hh = lane >> 5;  // MFMA column and half
+  const int hq = h0 + wave / C::WPH;
   const int q_first = i * BQ + (wave % C::WPH) * C::NQW;
   const Geo32 g = geo32(make_geo(p.n_q, p.n_k, p.w_sink, p.w_near, BQ, BK, p.h_k_offset + hk, p.h_k_total));
   const __bf16* kbase = k + ((int64_t)b * p.h_k + hk) * p.n_k * D;
   const __bf16* vbase = v + ((int64_t)b * p.h_k + hk) * p.n_k * D;
   const uint32_t smem_base = lds_addr(smem);
+
+  // zero the K/V buffers once: key rows past the end of the sequence are not
+  // copied (the buffer loads return zero there) and must hold finite values
+  for (int x = tid; x < C::MAIN_BYTES / 16; x += blockDim.x) reinterpret_cast<u32x4*>(smem)[x] = u32x4{0u, 0u, 0u, 0u};
 
   // the row's entries, split into full (from the front) and partial (from the back) lists
   const int r = hk * sv.n_qt + i;
@@ -138,236 +199,268 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
     const int idx = tt < n_full ? tt : cap - 1 - (tt - n_full);
     return __builtin_amdgcn_readfirstlane(list[idx]);
   };
-  // LDS: K of block t in K buffer t % 2, V of block t in V buffer t % 2
+
+  // Global -> LDS copies of K and V blocks.  With four waves each lane copies
+  // the same 16-byte column of its row in every 1 KB piece it takes; the block
+  // and piece positions go into the (scalar) buffer resource.
+  constexpr int RPL = 1024 / (D * 2);  // rows per 1 KB piece
+  constexpr int PPW = T::LOADS / 4;    // pieces per wave
+  uint32_t dma_off;
+  {
+    const int row0 = wave * RPL + lane / T::CH;
+    const int col = (lane % T::CH) ^ swz<T::CH>(row0);
+    dma_off = (uint32_t)((row0 * D + col * 8) * 2);
+  }
   auto kbuf_off = [](int t) { return (t & 1) * 2 * T::BYTES; };
   auto vbuf_off = [](int t) { return (t & 1) * 2 * T::BYTES + T::BYTES; };
-  auto stage_k = [&](int t) {
-    load_tile_asm_nw<D, BK>(kbase, (int)(entry_at(t) >> 1) * BK, p.n_k, smem_base + kbuf_off(t), wave, nw, lane);
-  };
-  auto stage_v = [&](int t) {
-    load_tile_asm_nw<D, BK>(vbase, (int)(entry_at(t) >> 1) * BK, p.n_k, smem_base + vbuf_off(t), wave, nw, lane);
-  };
-  __syncthreads();  // the lists are in LDS
-
-  // Q^T fragments (B operands): query column nt*16 + lr, d = ks*32 + 8*lg + 0..7
-  const int64_t row_base = ((int64_t)b * p.h_q + h) * p.n_q;
-  bf16x8 qf[NTQ][KSD];
+  auto stage = [&](const __bf16* base, int t, int buf_off) {
+    const int kf = (int)(entry_at(t) >> 1) * BK;
+    if constexpr (FOUR) {
 #pragma unroll
-  for (int nt = 0; nt < NTQ; ++nt) {
-    const int qp = q_first + nt * 16 + lr;
+      for (int n = 0; n < PPW; ++n) {
+        const int row = kf + n * 4 * RPL;  // first row of the piece round
+        const i32x4 rs = buffer_rsrc(base + (int64_t)row * D, p.n_k > row ? (uint32_t)(p.n_k - row) * D * 2 : 0u);
+        dma16_buf(dma_off, rs, smem_base + buf_off + (n * 4 + wave) * 1024);
+      }
+    } else {
+      load_tile_asm_nw<D, BK>(base, kf, p.n_k, smem_base + buf_off, wave, nw, lane);
+    }
+  };
+  // copies of one tile still in flight per thread when the next tile's are issued
+  __syncthreads();  // the lists and the zeroed buffers are in LDS
+
+  // Q^T fragments (B operands): query column 32 nq + l32, d = 16 ks + 8 hh + 0..7
+  const int64_t row_base = ((int64_t)b * p.h_q + hq) * p.n_q;
+  bf16x8 qf[NQT][KS];
+#pragma unroll
+  for (int nq = 0; nq < NQT; ++nq) {
+    const int qp = q_first + nq * 32 + l32;
     const bool ok = qp < p.n_q;
     const __bf16* qrow = q + (row_base + (ok ? qp : 0)) * D;
 #pragma unroll
-    for (int ks = 0; ks < KSD; ++ks) {
-      const bf16x8 val = *reinterpret_cast<const bf16x8*>(qrow + ks * 32 + 8 * lg);
-      qf[nt][ks] = ok ? val : bf16x8{};
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 val = *reinterpret_cast<const bf16x8*>(qrow + ks * 16 + 8 * hh);
+      qf[nq][ks] = ok ? val : bf16x8{};
     }
   }
-  f32x4 oacc[MTD][NTQ];  // O^T: rows d, columns queries
+  // LDS fragment offsets for chunk 0 of a tile (the swizzle depends on row % 16,
+  // so chunks 32 rows further and k-steps 16 rows further add plain row bytes)
+  //  K (A operand of S^T): row l32, columns 16 ks + 8 hh + 0..7;
+  //  V^T (A operand of O^T): transposing reads of rows 4 hh + (lane % 16) / 4
+  //  (+ 8 for slots 4..7), columns 32 md + 16 ((lane / 16) % 2) + 4 (lane % 4).
+  int offk[KS], offv[MD][2];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) offk[ks] = T::off(l32, 2 * ks + hh);
+#pragma unroll
+  for (int md = 0; md < MD; ++md)
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf)
+      offv[md][hf] = T::off_col(4 * hh + ((lane & 15) >> 2) + 8 * hf, 32 * md + 16 * ((lane >> 4) & 1) + 4 * (lane & 3));
+  auto ld_v = [&](const unsigned char* tile, int md, int row_bytes) -> bf16x8 {
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(tile + offv[md][0] + row_bytes));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(tile + offv[md][1] + row_bytes));
+    const bf16x4 a = __builtin_bit_cast(bf16x4, lo), c2 = __builtin_bit_cast(bf16x4, hi);
+    return bf16x8{a[0], a[1], a[2], a[3], c2[0], c2[1], c2[2], c2[3]};
+  };
+
+  // O^T accumulators: element (lane, e) is d = 32 md + 8 (e / 4) + 4 hh + e % 4, query 32 nq + l32
+  f32x16 oacc[MD][NQT];
+  // S^T of two chunks: element (lane, e) is key 8 (e / 4) + 4 hh + e % 4 of the
+  // chunk, query 32 nq + l32.  Slots e = 8 kk .. 8 kk + 7 are exactly the keys
+  // that lane holds in k-step kk of O^T += V^T P^T (16 keys each), so P^T needs
+  // no data movement.
+  f32x16 sacc[2][NQT];
+  u32x4 pbw[2][2][NQT];  // P^T of two chunks: bf16 pairs, [chunk % 2][k-step][query tile]
+
   // The exponent offset m (base 2, per query column) is fixed once per row:
   // the maximum over the first 32 keys of the row's first block.  P = exp2(s c - m)
-  // can then exceed 1, but O and l share the offset, so O / l and
-  // LSE = (m + log2 l) ln 2 are unaffected; no O rescaling is ever needed.  If a
-  // later score exceeds m by more than kLimit (P > 2^kLimit, where bf16 P and
-  // fp32 sums would approach their range), the workgroup runs the row again
-  // with m set to the row maximum found by the first pass.
+  // may exceed 1; O and l share the offset, so O / l and LSE = (m + log2 l) ln 2
+  // are unaffected and O never needs rescaling.  If a later score exceeds m by
+  // more than kLimit (P > 2^kLimit, where bf16 P and fp32 sums would approach
+  // their range), or m was unset, the workgroup runs the row again with m set
+  // to the row maximum found by the first pass.
   constexpr float kLimit = 64.f;
-  float m_fix[NTQ], m_hi[NTQ], l_run[NTQ], mu[NTQ];  // m_hi: this lane's maximum raw score per column
+  float m_fix[NQT], m_hi[NQT], l_run[NQT], mu[NQT];  // m_hi: this lane's maximum raw score per column
 #pragma unroll
-  for (int nt = 0; nt < NTQ; ++nt) m_fix[nt] = -INFINITY;
+  for (int nq = 0; nq < NQT; ++nq) m_fix[nq] = -INFINITY;
   const float c = p.softmax_scale * kLog2e;
-  int offr[KSD], offt[MTD];
-#pragma unroll
-  for (int ks = 0; ks < KSD; ++ks) offr[ks] = row8_off<D>(lr, lg, ks);
-#pragma unroll
-  for (int md = 0; md < MTD; ++md) offt[md] = tr8_off<D>(lr, lg, md);
+  const bf16x2 ones = {(__bf16)1.f, (__bf16)1.f};
 
-  // Software pipeline over the row's 32-key chunks.  While the matrix cores
-  // compute S^T of chunk n (K fragments of the current block) and O^T += V^T P^T
-  // of a chunk one block back (V fragments of the previous block), the vector
-  // ALUs turn S^T of chunk n - 1 into P^T: the two streams are independent, so
-  // the exponentials of the softmax hide under the products.
-  f32x4 sacc[2][2][NTQ];  // S^T of two chunks ([chunk % 2][16-key tile][query tile])
-  bf16x8 pb[NCH][NTQ];    // P^T of the chunks of one block, as B operands
-
-  // The softmax of one chunk is split into 32 element steps (element e: query
-  // tile e / 8, key tile (e / 4) % 2, row e % 4), spread evenly over NS slots
-  // of one MFMA each: first exponent, then sum, running maximum and packing.
   float pv[32];  // exponentials in flight between the two halves of an element step
+  // element step e of a chunk's softmax (query tile e / 16, slot e % 16), first half
   auto soft_a = [&](auto ec, auto rpc, bool masked, int key0) __attribute__((always_inline)) {
     constexpr int e = decltype(ec)::value, rp = decltype(rpc)::value;
-    constexpr int nt = e / 8, tt = (e / 4) % 2, rr = e % 4;
-    if (masked)
-      sacc[rp][tt][nt][rr] += legal32(g, q_first + nt * 16 + lr, key0 + tt * 16 + 4 * lg + rr) ? 0.f : -INFINITY;
-    pv[e] = __builtin_amdgcn_exp2f(fmaf(sacc[rp][tt][nt][rr], c, -mu[nt]));
+    constexpr int nq = e / 16, s = e % 16;
+    if (masked)  // key0: this lane's first key of the chunk
+      sacc[rp][nq][s] += legal32(g, q_first + nq * 32 + l32, key0 + 8 * (s >> 2) + (s & 3)) ? 0.f : -INFINITY;
+    pv[e] = __builtin_amdgcn_exp2f(fmaf(sacc[rp][nq][s], c, -mu[nq]));
   };
+  // second half (odd e): running maximum, bf16 pair, row sum
   auto soft_b = [&](auto ec, auto rpc, auto psc) __attribute__((always_inline)) {
     constexpr int e = decltype(ec)::value, rp = decltype(rpc)::value, ps = decltype(psc)::value;
-    constexpr int nt = e / 8, tt = (e / 4) % 2, rr = e % 4;
-    l_run[nt] += pv[e];
-    if constexpr (rr & 1) {
-      m_hi[nt] = max3(m_hi[nt], sacc[rp][tt][nt][rr - 1], sacc[rp][tt][nt][rr]);
-      pb[ps][nt][4 * tt + rr - 1] = (__bf16)pv[e - 1];
-      pb[ps][nt][4 * tt + rr] = (__bf16)pv[e];
+    constexpr int nq = e / 16, s = e % 16;
+    if constexpr (s & 1) {
+      m_hi[nq] = max3(m_hi[nq], sacc[rp][nq][s - 1], sacc[rp][nq][s]);
+      const bf16x2 pk = {(__bf16)pv[e - 1], (__bf16)pv[e]};
+      l_run[nq] = __builtin_amdgcn_fdot2_f32_bf16(pk, ones, l_run[nq], false);  // l from the rounded P
+      pbw[ps][s / 8][nq][(s & 7) >> 1] = __builtin_bit_cast(uint32_t, pk);
     }
   };
-  // the element steps of slot `slot` out of NS
+  // the element steps that belong to slot `slot` of NS
   auto soft_slot = [&](auto slotc, auto nsc, auto rpc, auto psc, bool masked, int key0) __attribute__((always_inline)) {
     constexpr int slot = decltype(slotc)::value, NS = decltype(nsc)::value;
-    constexpr int LAG = NS >= 64 ? NS / 64 : 0;  // slots between the two halves of an element step
     static_for<32>([&](auto ec) {
       constexpr int e = decltype(ec)::value;
       constexpr int sa = e * NS / 32;
+      constexpr int sb = sa + 1 < NS ? sa + 1 : sa;
       if constexpr (sa == slot) soft_a(ec, rpc, masked, key0);
-      if constexpr (sa + LAG == slot) soft_b(ec, rpc, psc);
+      if constexpr (sb == slot) soft_b(ec, rpc, psc);
     });
   };
 
-  // O^T += V^T P^T for chunk j of a block (V tile Vt) and S^T of chunk j (K tile
-  // Kt), group by group, fragments read PF groups ahead.  gi -> S group or O group.
-  constexpr int PF = 2;
+  // Software pipeline over the row's 32-key chunks: chunk n has its S^T
+  // computed in chunk step n, is exponentiated in step n + 1 and enters
+  // O^T += V^T P^T in step n + 2.  Within a chunk step the matrix cores work on
+  // S^T (chunk n) and O^T (chunk n - 2) while the vector ALUs turn S^T of chunk
+  // n - 1 into P^T: the streams are independent, so the exponentials hide under
+  // the products.  Fragments are read PF groups ahead.
+  //
+  // LDS: K of block t in K buffer t % 2, V of block t in V buffer t % 2.  The
+  // O^T products of block t's steps read V of block t - 1 for the chunks two
+  // back; with 128-key blocks, V of block t is needed from its third step on,
+  // so it is copied in the middle of block t - 1, once V of block t - 2 is no
+  // longer read.
+#ifndef FWD_PF
+#define FWD_PF 2
+#endif
+  constexpr int PF = FWD_PF, RING = PF + 2;
   int k_prev = 0;  // first key of the previous block
-  // One block of the pipeline.  FIRST: the row's first block (no previous block:
-  // no O^T products, no softmax before the first chunk).  MPREV / MCUR: the
-  // chunks softmaxed here from the previous / this block need the element mask.
+  // One block.  FIRST: the row's first block (nothing before its first chunk).
+  // MPREV / MCUR: the chunks exponentiated here from the previous / this block
+  // need the element mask.
   auto step = [&](int t, auto firstc, auto mprevc, auto mcurc) __attribute__((always_inline)) {
-    constexpr bool FIRST = decltype(firstc)::value, MPREV = decltype(mprevc)::value, MCUR = decltype(mcurc)::value;
+    constexpr bool FIRST = decltype(firstc)::value, MPREV = decltype(mprevc)::value;
+    constexpr bool MCUR = decltype(mcurc)::value;
     const int k_first = (int)(entry_at(t) >> 1) * BK;
-    if (t + 1 < n_ent) stage_k(t + 1);  // K buffer of block t - 1: free
-    stage_v(t);                         // V buffer of block t - 2: free
+    stage(kbase, t + 1, kbuf_off(t + 1));  // K buffer of block t - 1: free (the last block repeats itself)
+    if constexpr (NCH == 2) stage(vbase, t, vbuf_off(t));  // V buffer of block t - 2: free
     const unsigned char* Kt = smem + kbuf_off(t);
+    const unsigned char* Vt = smem + vbuf_off(t);
     const unsigned char* Vp = smem + vbuf_off(t + 1);  // V of block t - 1
     constexpr int NGS = NCH * NG;
-    bf16x8 fa[PF + 1];
+    bf16x8 fa[RING];
+    // group GG of the block: chunk step j, S^T k-step or O^T (k-step kk, d tile md)
     auto load = [&](auto gc, bf16x8& dst) __attribute__((always_inline)) {
       constexpr int GG = decltype(gc)::value, j = GG / NG, gi = GG % NG;
-      constexpr bool S = NCH >= 2 ? (gi % 2 == 0) : (gi < 2 * KSD);
-      constexpr int x = NCH >= 2 ? gi / 2 : (S ? gi : gi - 2 * KSD);
+      constexpr bool S = gi % 2 == 0;
+      constexpr int x = gi / 2;
+      constexpr int jo = (j + NCH - 2) % NCH;  // chunk of the O^T products within its block
+      constexpr bool OLD = j < 2;              // ... of the previous block
       if constexpr (S) {
-        dst = ld_row8(Kt + offr[x % KSD] + (j * 32 + (x / KSD) * 16) * D * 2);
-      } else if constexpr (!FIRST) {
-        dst = ld_tr8(Vp + offt[x] + j * 32 * D * 2, D * 2);
+        dst = ld_row8(Kt + offk[x] + j * 32 * D * 2);
+      } else if constexpr (!(FIRST && OLD)) {
+        constexpr int kk = x / MD, md = x % MD;
+        dst = ld_v(OLD ? Vp : Vt, md, (jo * 32 + kk * 16) * D * 2);
       }
     };
     static_for<PF>([&](auto ic) { load(ic, fa[decltype(ic)::value]); });
     __builtin_amdgcn_sched_barrier(0);
     static_for<NGS>([&](auto gc) {
       constexpr int GG = decltype(gc)::value, j = GG / NG, gi = GG % NG;
-      constexpr bool S = NCH >= 2 ? (gi % 2 == 0) : (gi < 2 * KSD);
-      constexpr int x = NCH >= 2 ? gi / 2 : (S ? gi : gi - 2 * KSD);
-      if constexpr (GG + PF < NGS) load(std::integral_constant<int, GG + PF>{}, fa[(GG + PF) % (PF + 1)]);
-      const bf16x8& a = fa[GG % (PF + 1)];
-      // the softmax of the chunk before chunk j: chunk j - 1 of this block, or
-      // the last chunk of the previous block; spread over all groups, or for a
-      // one-chunk block over the S groups (its P^T is consumed within the block)
-      constexpr int NS = NCH >= 2 ? 4 * NG : 4 * 2 * KSD;
-      constexpr int ps = (j + NCH - 1) % NCH;
-      static_for<NTQ>([&](auto mc) {
+      constexpr bool S = gi % 2 == 0;
+      constexpr int x = gi / 2;
+      constexpr bool OLD = j < 2;
+      if constexpr (NCH == 4 && GG == 2 * NG - PF) {
+        // middle of a 128-key block, before the first read of V of block t
+        // (fragments run PF groups ahead) and after the last read of V of
+        // block t - 1 was issued: V of block t is in (its copies were issued
+        // before this block's K copies), and once every wave's reads of V of
+        // block t - 1 are done, the copy of block t + 1 may overwrite it
+        if constexpr (FOUR)
+          __builtin_amdgcn_s_waitcnt(vmcnt_only(PPW));
+        else
+          __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        stage(vbase, t + 1, vbuf_off(t + 1));
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if constexpr (GG + PF < NGS) load(std::integral_constant<int, GG + PF>{}, fa[(GG + PF) % RING]);
+      const bf16x8& a = fa[GG % RING];
+      static_for<NQT>([&](auto mc) {
         constexpr int m = decltype(mc)::value;
         if constexpr (S) {
-          constexpr int tt = x / KSD, ks = x % KSD;
-          if constexpr (ks == 0)
-            sacc[j & 1][tt][m] = mfma_v0(a, qf[m][ks]);
+          if constexpr (x == 0)
+            sacc[j & 1][m] = mfma32_v0(a, qf[m][0]);
           else
-            sacc[j & 1][tt][m] = mfma_v(a, qf[m][ks], sacc[j & 1][tt][m]);
-        } else if constexpr (!FIRST) {
-          oacc[x][m] = mfma16(a, pb[j][m], oacc[x][m]);
+            sacc[j & 1][m] = mfma32_v(a, qf[m][x], sacc[j & 1][m]);
+        } else if constexpr (!(FIRST && OLD)) {
+          constexpr int kk = x / MD, md = x % MD;
+          oacc[md][m] = mfma32(a, __builtin_bit_cast(bf16x8, pbw[j & 1][kk][m]), oacc[md][m]);
         }
-        constexpr int slot = gi * NTQ + m;
-        if constexpr (!(FIRST && j == 0) && slot < NS) {
+        // the softmax of the chunk before chunk j (chunk j - 1 of this block,
+        // or the last chunk of the previous block), spread over the products
+        constexpr int slot = gi * NQT + m;
+        if constexpr (!(FIRST && j == 0)) {
           using SL = std::integral_constant<int, slot>;
-          using NSC = std::integral_constant<int, NS>;
-          using PS = std::integral_constant<int, ps>;
+          using NSC = std::integral_constant<int, NQT * NG>;
+          using RP = std::integral_constant<int, (j + 1) & 1>;
           if constexpr (j == 0)
-            soft_slot(SL{}, NSC{}, std::integral_constant<int, 1>{}, PS{}, MPREV, k_prev + (NCH - 1) * 32);
+            soft_slot(SL{}, NSC{}, RP{}, RP{}, MPREV, k_prev + (NCH - 1) * 32 + 4 * hh);
           else
-            soft_slot(SL{}, NSC{}, std::integral_constant<int, (j + 1) & 1>{}, PS{}, MCUR, k_first + (j - 1) * 32);
+            soft_slot(SL{}, NSC{}, RP{}, RP{}, MCUR, k_first + (j - 1) * 32 + 4 * hh);
         }
         __builtin_amdgcn_sched_barrier(0);
       });
+      // a chunk step without O^T products (start of the row): its S^T results
+      // are read early in the next step, so settle them here
+      if constexpr (FIRST && OLD && gi == NG - 1) {
+        mfma_settle(sacc[j & 1][0], sacc[j & 1][1]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     });
-    // the last S^T products of the block may still be in flight (a first block
-    // has no O^T products after them): 16 wait states before anything reads them
-    asm volatile("s_nop 7\n\ts_nop 7");
+    // the last S^T products may still be in flight: wait states before
+    // anything reads them
+    mfma_settle(sacc[1][0], sacc[1][1]);
     __builtin_amdgcn_sched_barrier(0);
-    if constexpr (NCH == 1) {
-#pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-        for (int nt = 0; nt < NTQ; ++nt) sacc[1][tt][nt] = sacc[0][tt][nt];
-    }
     // register placement: O^T accumulators and Q^T fragments in AGPRs (read
     // directly by the matrix cores), S^T and P^T in VGPRs; these emit nothing
 #pragma unroll
-    for (int md = 0; md < MTD; ++md)
+    for (int md = 0; md < MD; ++md)
 #pragma unroll
-      for (int nt = 0; nt < NTQ; ++nt) asm volatile("" : "+" FWD_OPIN(oacc[md][nt]));
+      for (int nq = 0; nq < NQT; ++nq) asm volatile("" : "+a"(oacc[md][nq]));
 #pragma unroll
-    for (int nt = 0; nt < NTQ; ++nt)
+    for (int nq = 0; nq < NQT; ++nq)
 #pragma unroll
-      for (int ks = 0; ks < KSD; ++ks) asm volatile("" : "+" FWD_QPIN(qf[nt][ks]));
+      for (int ks = 0; ks < KS; ++ks) asm volatile("" : "+a"(qf[nq][ks]));
     k_prev = k_first;
-    __builtin_amdgcn_s_waitcnt(0);  // block t + 1's K and block t's V have landed
-    __syncthreads();                 // ... for every wave, and the freed buffers are no longer read
+    // the next block's K has landed (with 128-key blocks the next V may still
+    // be in flight)
+    if constexpr (NCH == 4 && FOUR)
+      __builtin_amdgcn_s_waitcnt(vmcnt_only(PPW));
+    else
+      __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();  // ... for every wave, and the freed buffers are no longer read
   };
-  // after the last block: the softmax of its last chunk, then its O^T products
+  // after the last block: the softmax of its last chunk, then the O^T products
+  // of its last two chunks
   auto drain = [&](int t) __attribute__((always_inline)) {
     using R1 = std::integral_constant<int, 1>;
-    static_for<32>([&](auto ec) { soft_a(ec, R1{}, true, k_prev + (NCH - 1) * 32); });
-    static_for<32>([&](auto ec) { soft_b(ec, R1{}, std::integral_constant<int, NCH - 1>{}); });
+    static_for<32>([&](auto ec) { soft_a(ec, R1{}, true, k_prev + (NCH - 1) * 32 + 4 * hh); });
+    static_for<32>([&](auto ec) { soft_b(ec, R1{}, R1{}); });
+    if constexpr (NCH == 4 && FOUR) __builtin_amdgcn_s_waitcnt(0);  // (the repeated V copy of the mid-block)
     const unsigned char* Vt = smem + vbuf_off(t);
-    static_for<NCH * MTD>([&](auto gc) {
-      constexpr int GG = decltype(gc)::value, j = GG / MTD, md = GG % MTD;
-      const bf16x8 a = ld_tr8(Vt + offt[md] + j * 32 * D * 2, D * 2);
+    static_for<2 * 2 * MD>([&](auto gc) {
+      constexpr int GG = decltype(gc)::value, jj = GG / (2 * MD), kk = (GG / MD) % 2, md = GG % MD;
+      constexpr int jo = NCH - 2 + jj;  // chunk within the block
+      const bf16x8 a = ld_v(Vt, md, (jo * 32 + kk * 16) * D * 2);
 #pragma unroll
-      for (int nt = 0; nt < NTQ; ++nt) oacc[md][nt] = mfma16(a, pb[j][nt], oacc[md][nt]);
+      for (int nq = 0; nq < NQT; ++nq)
+        oacc[md][nq] = mfma32(a, __builtin_bit_cast(bf16x8, pbw[jo & 1][kk][nq]), oacc[md][nq]);
     });
   };
-
-  for (int pass = 0; pass < 2; ++pass) {
-#pragma unroll
-    for (int nt = 0; nt < NTQ; ++nt) {
-      m_hi[nt] = -INFINITY;
-      l_run[nt] = 0.f;
-#pragma unroll
-      for (int md = 0; md < MTD; ++md) oacc[md][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-    if (n_ent > 0) stage_k(0);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (pass == 0 && n_ent > 0) {
-      // offsets from the first 32 keys of the row's first block (in processing
-      // order: a full block when the row has one; its first key is legal for
-      // every query of a causal row either way)
-      const int key0 = (int)(entry_at(0) >> 1) * BK;
-#pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-        for (int ks = 0; ks < KSD; ++ks) {
-          const bf16x8 a = ld_row8(smem + offr[ks] + tt * 16 * D * 2);
-#pragma unroll
-          for (int nt = 0; nt < NTQ; ++nt)
-            sacc[0][tt][nt] = mfma16(a, qf[nt][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sacc[0][tt][nt]);
-        }
-#pragma unroll
-      for (int nt = 0; nt < NTQ; ++nt) {
-        float cm = -INFINITY;
-#pragma unroll
-        for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-          for (int rr = 0; rr < 4; ++rr) {
-            const float sv2 = sacc[0][tt][nt][rr] + (legal32(g, q_first + nt * 16 + lr, key0 + tt * 16 + 4 * lg + rr) ? 0.f : -INFINITY);
-            cm = fmaxf(cm, sv2);
-          }
-        cm = fmaxf(cm, __shfl_xor(cm, 16));
-        cm = fmaxf(cm, __shfl_xor(cm, 32));
-        m_fix[nt] = cm * c;  // -inf for a column without a legal key there
-      }
-    }
-#pragma unroll
-    for (int nt = 0; nt < NTQ; ++nt) mu[nt] = m_fix[nt] == -INFINITY ? 0.f : m_fix[nt];
-    using TT = std::true_type;
-    using FF = std::false_type;
+  using TT = std::true_type;
+  using FF = std::false_type;
+  auto sweep = [&]() __attribute__((always_inline)) {
     int t = 0;
     if (n_full > 0) {
       step(0, TT{}, FF{}, FF{});
@@ -381,19 +474,60 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
       for (; t < n_ent; ++t) step(t, FF{}, TT{}, TT{});
     }
     if (n_ent > 0) drain(n_ent - 1);
+  };
+
+  int* vote = reinterpret_cast<int*>(smem + C::MAIN_BYTES + 4 * cap);
+  for (int pass = 0; pass < 2; ++pass) {
+#pragma unroll
+    for (int nq = 0; nq < NQT; ++nq) {
+      m_hi[nq] = -INFINITY;
+      l_run[nq] = 0.f;
+#pragma unroll
+      for (int md = 0; md < MD; ++md) oacc[md][nq] = f32x16{};
+    }
+    if (n_ent > 0) {
+      stage(kbase, 0, kbuf_off(0));
+      if (NCH == 4) stage(vbase, 0, vbuf_off(0));  // (needed from the block's third chunk)
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (pass == 0 && n_ent > 0) {
+      // offsets from the first 32 keys of the row's first block (in processing
+      // order: a full block when the row has one)
+      const int kb = (int)(entry_at(0) >> 1) * BK + 4 * hh;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8 a = ld_row8(smem + offk[ks]);
+#pragma unroll
+        for (int nq = 0; nq < NQT; ++nq)
+          sacc[0][nq] = ks == 0 ? mfma32_v0(a, qf[nq][0]) : mfma32_v(a, qf[nq][ks], sacc[0][nq]);
+        mfma_settle(sacc[0][0], sacc[0][1]);  // the next k-step reads these accumulators
+      }
+#pragma unroll
+      for (int nq = 0; nq < NQT; ++nq) {
+        float cm = -INFINITY;
+#pragma unroll
+        for (int x = 0; x < 16; ++x) {
+          const bool ok = legal32(g, q_first + nq * 32 + l32, kb + 8 * (x >> 2) + (x & 3));
+          cm = fmaxf(cm, ok ? sacc[0][nq][x] : -INFINITY);
+        }
+        cm = fmaxf(cm, __shfl_xor(cm, 32));
+        m_fix[nq] = cm * c;  // -inf for a column without a legal key there
+      }
+    }
+#pragma unroll
+    for (int nq = 0; nq < NQT; ++nq) mu[nq] = m_fix[nq] == -INFINITY ? 0.f : m_fix[nq];
+    sweep();
     // did a score exceed its column's offset by more than kLimit?
     bool far = false;
 #pragma unroll
-    for (int nt = 0; nt < NTQ; ++nt) {
-      float cm = m_hi[nt];
-      cm = fmaxf(cm, __shfl_xor(cm, 16));
-      cm = fmaxf(cm, __shfl_xor(cm, 32));
-      m_hi[nt] = cm * c;  // the column's maximum, in exponent units
+    for (int nq = 0; nq < NQT; ++nq) {
+      const float mh = fmaxf(m_hi[nq], __shfl_xor(m_hi[nq], 32)) * c;  // the column maximum, exponent units
       // (a column whose offset is unset but which met legal keys later is run again too)
-      far |= m_hi[nt] != -INFINITY && (m_fix[nt] == -INFINITY || m_hi[nt] > m_fix[nt] + kLimit);
+      far |= mh != -INFINITY && (m_fix[nq] == -INFINITY || mh > m_fix[nq] + kLimit);
+      m_fix[nq] = mh;  // the offset of a second pass: then P <= 1 everywhere
     }
     // workgroup vote through a word past the block lists
-    int* vote = reinterpret_cast<int*>(smem + C::MAIN_BYTES + 4 * cap);
     if (tid == 0) *vote = 0;
     __syncthreads();
     if (far) *vote = 1;
@@ -401,38 +535,34 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
     const bool again = *vote != 0;
     __syncthreads();
     if (!again) break;
-    // run the row again with the row maxima as offsets (then P <= 1 everywhere)
-#pragma unroll
-    for (int nt = 0; nt < NTQ; ++nt) m_fix[nt] = m_hi[nt];
   }
 
-  // O = O / l; LSE = (m + log2 l) ln 2 (m already in base-2 units)
+  // O = O / l; LSE = (m + log2 l) ln 2 with the offset m of the last pass (base 2)
 #pragma unroll
-  for (int nt = 0; nt < NTQ; ++nt) {
-    float lt = l_run[nt];
-    lt += __shfl_xor(lt, 16);
-    lt += __shfl_xor(lt, 32);
-    const int qp = q_first + nt * 16 + lr;
+  for (int nq = 0; nq < NQT; ++nq) {
+    const float lt = l_run[nq] + __shfl_xor(l_run[nq], 32);
+    const int qp = q_first + nq * 32 + l32;
     if (qp >= p.n_q) continue;
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
     __bf16* orow = o + (row_base + qp) * D;
 #pragma unroll
-    for (int md = 0; md < MTD; ++md) {
-      bf16x4 ov;
+    for (int md = 0; md < MD; ++md)
 #pragma unroll
-      for (int rr = 0; rr < 4; ++rr) ov[rr] = (__bf16)(oacc[md][nt][rr] * inv);
-      *reinterpret_cast<bf16x4*>(orow + md * 16 + 4 * lg) = ov;
-    }
-    if (lg == 0) lse[row_base + qp] = lt > 0.f ? (m_fix[nt] + __log2f(lt)) * kLn2 : -INFINITY;
+      for (int j4 = 0; j4 < 4; ++j4) {
+        bf16x4 ov;
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) ov[rr] = (__bf16)(oacc[md][nq][4 * j4 + rr] * inv);
+        *reinterpret_cast<bf16x4*>(orow + md * 32 + 8 * j4 + 4 * hh) = ov;
+      }
+    if (hh == 0) lse[row_base + qp] = lt > 0.f ? (mu[nq] + __log2f(lt)) * kLn2 : -INFINITY;
   }
 }
 
-template <int D, int BQ, int BK>
-hipError_t launch_cfg(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
-                      void* o, float* lse, hipStream_t stream) {
+template <int D, int BQ, int BK, bool FOUR>
+hipError_t launch_waves(const cowa_params& p, const SchedView& sv, int hpw, int n_hgroups, int waves, const void* q,
+                        const void* k, const void* v, void* o, float* lse, hipStream_t stream) {
   using C = FwdCfg<D, BQ, BK>;
-  if (sv.n_kt > C::max_kblocks()) return hipErrorInvalidValue;
-  auto kern = fwd_bf16_kernel<D, BQ, BK>;
+  auto kern = fwd_bf16_kernel<D, BQ, BK, FOUR>;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -440,11 +570,6 @@ hipError_t launch_cfg(const cowa_params& p, const SchedView& sv, const void* q, 
     if (err != hipSuccess) return err;
     attr_set = true;
   }
-  const int G = p.h_q / p.h_k;
-  int hpw = 256 / BQ;  // QO heads per workgroup: up to 256 query rows (four waves)
-  while (hpw > 1 && G % hpw != 0) hpw >>= 1;
-  const int n_hgroups = p.h_q / hpw;
-  const int waves = hpw * C::WPH;
   const unsigned blocks = (unsigned)sv.n_qt * n_hgroups * p.batch;
   hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * waves), C::lds_bytes(sv.n_kt), stream, p, sv, hpw, n_hgroups,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), static_cast<const __bf16*>(v),
@@ -452,17 +577,29 @@ hipError_t launch_cfg(const cowa_params& p, const SchedView& sv, const void* q, 
   return hipGetLastError();
 }
 
+template <int D, int BQ, int BK>
+hipError_t launch_cfg(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
+                      void* o, float* lse, hipStream_t stream) {
+  using C = FwdCfg<D, BQ, BK>;
+  if (sv.n_kt > C::max_kblocks()) return hipErrorInvalidValue;
+  const int G = p.h_q / p.h_k;
+  int hpw = 256 / BQ;  // QO heads per workgroup: up to 256 query rows (four waves)
+  while (hpw > 1 && G % hpw != 0) hpw >>= 1;
+  const int n_hgroups = p.h_q / hpw;
+  const int waves = hpw * C::WPH;
+  if (waves == 4) return launch_waves<D, BQ, BK, true>(p, sv, hpw, n_hgroups, waves, q, k, v, o, lse, stream);
+  return launch_waves<D, BQ, BK, false>(p, sv, hpw, n_hgroups, waves, q, k, v, o, lse, stream);
+}
+
 }  // namespace
 
 int fwd_bf16_max_kblocks(int d, int tk) {
-  if (d == 128) return tk == 128 ? FwdCfg<128, 128, 128>::max_kblocks() : tk == 64 ? FwdCfg<128, 128, 64>::max_kblocks()
-                                                                                 : FwdCfg<128, 128, 32>::max_kblocks();
-  return tk == 128 ? FwdCfg<64, 128, 128>::max_kblocks() : tk == 64 ? FwdCfg<64, 128, 64>::max_kblocks()
-                                                                     : FwdCfg<64, 128, 32>::max_kblocks();
+  if (d == 128) return tk == 128 ? FwdCfg<128, 128, 128>::max_kblocks() : FwdCfg<128, 128, 64>::max_kblocks();
+  return tk == 128 ? FwdCfg<64, 128, 128>::max_kblocks() : FwdCfg<64, 128, 64>::max_kblocks();
 }
 
 bool fwd_bf16_supported(int d, int tq, int tk) {
-  return (d == 64 || d == 128) && (tq == 64 || tq == 128) && (tk == 32 || tk == 64 || tk == 128);
+  return (d == 64 || d == 128) && (tq == 64 || tq == 128) && (tk == 64 || tk == 128);
 }
 
 hipError_t launch_fwd_bf16(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
@@ -471,16 +608,12 @@ hipError_t launch_fwd_bf16(const cowa_params& p, const SchedView& sv, const void
   if (p.head_dim == D_ && p.tile_q == BQ_ && p.tile_k == BK_) return launch_cfg<D_, BQ_, BK_>(p, sv, q, k, v, o, lse, stream);
   COWA_FWD_CASE(128, 128, 128)
   COWA_FWD_CASE(128, 128, 64)
-  COWA_FWD_CASE(128, 128, 32)
   COWA_FWD_CASE(128, 64, 128)
   COWA_FWD_CASE(128, 64, 64)
-  COWA_FWD_CASE(128, 64, 32)
   COWA_FWD_CASE(64, 128, 128)
   COWA_FWD_CASE(64, 128, 64)
-  COWA_FWD_CASE(64, 128, 32)
   COWA_FWD_CASE(64, 64, 128)
   COWA_FWD_CASE(64, 64, 64)
-  COWA_FWD_CASE(64, 64, 32)
 #undef COWA_FWD_CASE
   return hipErrorInvalidValue;
 }

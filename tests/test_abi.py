@@ -135,6 +135,11 @@ def test_fwd_argument_errors_on_host():
     p32.tile_q = 32
     s32 = _sized(p32)
     assert lib.cowa_fwd(ctypes.byref(p32), ctypes.byref(s32), *[vp(ok)] * 5, vp(0)) == abi.COWA_ERR_UNSUPPORTED
+    # ... nor with a 32-key block
+    k32 = _good()
+    k32.tile_k = 32
+    sk32 = _sized(k32)
+    assert lib.cowa_fwd(ctypes.byref(k32), ctypes.byref(sk32), *[vp(ok)] * 5, vp(0)) == abi.COWA_ERR_UNSUPPORTED
 
 
 def test_batch_zero_is_a_no_op():

@@ -54,7 +54,7 @@ ODD = [
     ("ragged", 2, 333, 333, 4, 2, 128, 5, 40, 64, 64, "bf16", 0, 0),
     ("chunked_prefill", 1, 200, 1111, 8, 2, 128, 16, 100, 128, 128, "bf16", 0, 0),
     ("gqa8", 1, 1000, 1000, 8, 1, 64, 3, 77, 128, 64, "bf16", 0, 0),
-    ("mha", 1, 700, 700, 3, 3, 128, 0, 50, 64, 32, "bf16", 0, 0),
+    ("mha", 1, 700, 700, 3, 3, 128, 0, 50, 64, 64, "bf16", 0, 0),
     ("tp_rank", 1, 2048, 2048, 4, 1, 128, 32, 256, 128, 128, "bf16", 8, 5),
     ("dense", 1, 777, 777, 4, 2, 128, 0, 777, 128, 128, "bf16", 0, 0),
     ("wide_windows", 1, 500, 500, 2, 2, 64, 400, 400, 64, 128, "bf16", 0, 0),
