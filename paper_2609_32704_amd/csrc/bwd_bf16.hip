@@ -93,11 +93,12 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
   using C = BwdCfg<D, BK, NW>;
   extern __shared__ __align__(1024) unsigned char smem[];
 
-  const int total = sv.n_kt * p.h_k * p.batch;
-  const int work = xcd_remap(blockIdx.x, total);
-  const int j = work % sv.n_kt;  // KV block (sink blocks, with the longest query lists, first)
-  const int hk = (work / sv.n_kt) % p.h_k;
-  const int b = work / (sv.n_kt * p.h_k);
+  // clusters of 32 consecutive KV blocks of one KV head share an XCD's L2;
+  // first blocks (the sink, with the longest query lists) first
+  const WorkItem wi = cluster_item(blockIdx.x, sv.n_kt, 1, p.batch * p.h_k, 32, false);
+  const int j = wi.row;
+  const int hk = wi.unit % p.h_k;
+  const int b = wi.unit / p.h_k;
   const int G = p.h_q / p.h_k;
   const Geo32 g = geo32(make_geo(p.n_q, p.n_k, p.w_sink, p.w_near, p.tile_q, BK, p.h_k_offset + hk, p.h_k_total));
 
@@ -462,13 +463,12 @@ __global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, S
 
   const int nw = blockDim.x >> 6;
   const int G = p.h_q / p.h_k;
-  const int total = sv.n_qt * n_hgroups * p.batch;
-  const int work = xcd_remap(blockIdx.x, total);
-  const int per_i = n_hgroups * p.batch;
-  const int i = sv.n_qt - 1 - work / per_i;  // latest (longest) QO blocks first
-  const int rest = work % per_i;
-  const int hgi = rest % n_hgroups, b = rest / n_hgroups;
-  const int hk = hgi / (G / hpw);
+  // rows of 16 QO blocks x the head groups of one KV head share an XCD's L2;
+  // latest (longest) QO blocks first
+  const WorkItem wi = cluster_item(blockIdx.x, sv.n_qt, G / hpw, p.batch * p.h_k, 16, true);
+  const int i = wi.row, b = wi.unit / p.h_k;
+  const int hk = wi.unit % p.h_k;
+  const int hgi = hk * (G / hpw) + wi.group;
   const int h0 = hgi * hpw;
 
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;

@@ -88,41 +88,6 @@ __device__ inline void dma16_buf(uint32_t voff, i32x4 rsrc, uint32_t lds_base) {
                : "memory", "m0");
 }
 
-// Workgroup -> (QO block i, head group, sequence).  Workgroups are handed to
-// the 8 XCDs round-robin by id, and each XCD has its own L2.  Work is cut into
-// clusters of 16 consecutive QO blocks x the head groups of one KV head: those
-// rows walk nearly the same K/V blocks, so an XCD running one cluster at a time
-// (32 workgroups with two head groups per KV head) serves most block copies
-// from its L2.  Clusters go out latest QO blocks first (the longest rows), and
-// the KV head of an XCD's cluster rotates from one range of QO blocks to the
-// next, so every XCD gets the same mix of short- and long-window heads.
-// Shapes that do not tile this way keep a plain order with chunks of 8
-// consecutive items per XCD.
-__device__ inline void fwd_work_item(int id, int n_qt, int n_hgroups, int batch, int h_k, int* i, int* hgi, int* b) {
-  constexpr int CQ = 16;
-  const int hg_per_hk = n_hgroups / h_k;
-  const int units = batch * h_k;                // (sequence, KV head) pairs
-  const int n_clusters = units * (n_qt / CQ);
-  const int cs = CQ * hg_per_hk;                // workgroups per cluster
-  if (n_qt % CQ == 0 && n_clusters % 8 == 0) {
-    const int xcd = id & 7, n = id >> 3;
-    const int c = (n / cs) * 8 + xcd, item = n % cs;
-    const int r = c / units;
-    const int u = (c % units + r) % units;
-    *b = u / h_k;
-    *hgi = (u % h_k) * hg_per_hk + item % hg_per_hk;
-    *i = n_qt - 1 - (r * CQ + item / hg_per_hk);
-    return;
-  }
-  const int total = n_qt * n_hgroups * batch;
-  const int work = xcd_remap(id, total);
-  const int per_i = n_hgroups * batch;
-  *i = n_qt - 1 - work / per_i;
-  const int rest = work % per_i;
-  *hgi = rest % n_hgroups;
-  *b = rest / n_hgroups;
-}
-
 template <int D, int BQ, int BK>
 struct FwdCfg {
   static constexpr int NQW = 64;          // query rows per wave
@@ -155,9 +120,12 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
 
   const int nw = blockDim.x >> 6;
   const int G = p.h_q / p.h_k;
-  int i, hgi, b;
-  fwd_work_item(blockIdx.x, sv.n_qt, n_hgroups, p.batch, p.h_k, &i, &hgi, &b);
-  const int hk = hgi / (G / hpw);
+  // rows of 16 QO blocks x the head groups of one KV head share an XCD's L2;
+  // latest (longest) QO blocks first
+  const WorkItem wi = cluster_item(blockIdx.x, sv.n_qt, G / hpw, p.batch * p.h_k, 16, true);
+  const int i = wi.row, b = wi.unit / p.h_k;
+  const int hk = wi.unit % p.h_k;
+  const int hgi = hk * (G / hpw) + wi.group;
   const int h0 = hgi * hpw;  // first QO head of this workgroup (all in KV group hk)
 
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;

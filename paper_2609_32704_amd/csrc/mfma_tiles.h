@@ -44,6 +44,40 @@ __device__ inline int xcd_remap(int id, int total) {
   return chunk * 8 + (slot & 7);
 }
 
+// Workgroup id -> (row, group, unit) for a grid of n_rows x units x groups
+// workgroups, where the groups of one unit (one sequence and KV head) and
+// neighbouring rows read nearly the same K/V (or Q/dO) blocks.  Work is cut into
+// clusters of cq consecutive rows x the groups of one unit; cluster c runs on
+// XCD c % 8, so the workgroups an XCD runs together (one cluster) share its L2.
+// Rows go out first to last, or last to first (descending), whole cluster rows
+// at a time; the unit of an XCD's cluster rotates from one row range to the
+// next, so every XCD gets the same mix of units.  Shapes that do not tile this
+// way use the row order with chunks of 8 consecutive items per XCD.
+struct WorkItem {
+  int row, group, unit;
+};
+__device__ inline WorkItem cluster_item(int id, int n_rows, int groups, int units, int cq, bool descending) {
+  WorkItem w;
+  const int n_clusters = units * (n_rows / cq);
+  if (n_rows % cq == 0 && n_clusters % 8 == 0) {
+    const int cs = cq * groups;  // workgroups per cluster
+    const int xcd = id & 7, n = id >> 3;
+    const int c = (n / cs) * 8 + xcd, item = n % cs;
+    const int r = c / units;
+    w.unit = (c % units + r) % units;
+    w.group = item % groups;
+    w.row = r * cq + item / groups;
+  } else {
+    const int per_row = groups * units;
+    const int work = xcd_remap(id, n_rows * per_row);
+    w.row = work / per_row;
+    w.unit = (work % per_row) / groups;
+    w.group = work % groups;
+  }
+  if (descending) w.row = n_rows - 1 - w.row;
+  return w;
+}
+
 // XOR applied to the 16-byte chunk index of a row; depends on row % 16 only.
 // A read of 16 lanes covers 256 bytes; the choice below keeps every such read
 // of the two patterns on distinct four-byte banks whether the LDS serves 128
