@@ -31,6 +31,8 @@
 namespace cowa {
 namespace {
 
+
+
 // D[row] = sum_d O[row, d] dO[row, d], D/8 lanes per row.
 template <int D>
 __global__ void __launch_bounds__(256) bwd_pre(const __bf16* __restrict__ o, const __bf16* __restrict__ d_o,

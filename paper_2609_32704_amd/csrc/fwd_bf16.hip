@@ -64,6 +64,14 @@ __device__ inline f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& 
 __device__ inline void mfma_settle(f32x16& a, f32x16& b) {
   asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(a), "+v"(b));
 }
+__device__ inline void mfma_settle(f32x16& a) { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(a)); }
+template <int N>
+__device__ inline void mfma_settle(f32x16 (&r)[N]) {
+  if constexpr (N == 1)
+    mfma_settle(r[0]);
+  else
+    mfma_settle(r[0], r[1]);
+}
 
 // max(a, b, c) in one instruction (fmaxf would first quiet each operand that
 // the compiler cannot prove canonical: the products above are opaque to it)
@@ -91,6 +99,7 @@ __device__ inline void dma16_buf(uint32_t voff, i32x4 rsrc, uint32_t lds_base) {
 template <int D, int BQ, int BK>
 struct FwdCfg {
   static constexpr int NQW = 64;          // query rows per wave
+  static constexpr int NWF = 256 / NQW;   // waves of a full workgroup (256 query rows)
   static constexpr int NQT = NQW / 32;    // 32-query tiles per wave (columns of S^T)
   static constexpr int KS = D / 16;       // k-steps over d of S^T = K Q^T
   static constexpr int MD = D / 32;       // 32-row d tiles of O^T
@@ -106,9 +115,9 @@ struct FwdCfg {
   static_assert(NCH == 2 || NCH == 4, "64- or 128-key blocks");
 };
 
-// FOUR: launched with four waves (the fast copy path; a compile-time choice
+// FULL: launched with NWF waves (the fast copy path; a compile-time choice
 // keeps the block step free of branches)
-template <int D, int BQ, int BK, bool FOUR>
+template <int D, int BQ, int BK, bool FULL>
 __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView sv, int hpw, int n_hgroups,
                                                        const __bf16* __restrict__ q, const __bf16* __restrict__ k,
                                                        const __bf16* __restrict__ v, __bf16* __restrict__ o,
@@ -169,32 +178,32 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   };
 
   // Global -> LDS copies of K and V blocks.  With four waves each lane copies
-  // the same 16-byte column of its row in every 1 KB piece it takes; the block
-  // and piece positions go into the (scalar) buffer resource.
+  // the same 16-byte column of its row in every 1 KB piece it takes: its byte
+  // offsets within a block are fixed, and the block position goes into the
+  // (scalar) buffer resource, whose size bounds the reads to the sequence.
   constexpr int RPL = 1024 / (D * 2);  // rows per 1 KB piece
-  constexpr int PPW = T::LOADS / 4;    // pieces per wave
-  uint32_t dma_off;
+  constexpr int NWF = C::NWF;
+  constexpr int PPW = T::LOADS / NWF;  // pieces per wave
+  uint32_t dma_off[PPW];
   {
     const int row0 = wave * RPL + lane / T::CH;
     const int col = (lane % T::CH) ^ swz<T::CH>(row0);
-    dma_off = (uint32_t)((row0 * D + col * 8) * 2);
+#pragma unroll
+    for (int n = 0; n < PPW; ++n) dma_off[n] = (uint32_t)(((n * NWF * RPL + row0) * D + col * 8) * 2);
   }
   auto kbuf_off = [](int t) { return (t & 1) * 2 * T::BYTES; };
   auto vbuf_off = [](int t) { return (t & 1) * 2 * T::BYTES + T::BYTES; };
   auto stage = [&](const __bf16* base, int t, int buf_off) {
     const int kf = (int)(entry_at(t) >> 1) * BK;
-    if constexpr (FOUR) {
+    if constexpr (FULL) {
+      const i32x4 rs = buffer_rsrc(base + (int64_t)kf * D, (uint32_t)(p.n_k - kf) * D * 2);
+      const uint32_t lds0 = smem_base + buf_off + wave * 1024;
 #pragma unroll
-      for (int n = 0; n < PPW; ++n) {
-        const int row = kf + n * 4 * RPL;  // first row of the piece round
-        const i32x4 rs = buffer_rsrc(base + (int64_t)row * D, p.n_k > row ? (uint32_t)(p.n_k - row) * D * 2 : 0u);
-        dma16_buf(dma_off, rs, smem_base + buf_off + (n * 4 + wave) * 1024);
-      }
+      for (int n = 0; n < PPW; ++n) dma16_buf(dma_off[n], rs, lds0 + n * NWF * 1024);
     } else {
       load_tile_asm_nw<D, BK>(base, kf, p.n_k, smem_base + buf_off, wave, nw, lane);
     }
   };
-  // copies of one tile still in flight per thread when the next tile's are issued
   __syncthreads();  // the lists and the zeroed buffers are in LDS
 
   // Q^T fragments (B operands): query column 32 nq + l32, d = 16 ks + 8 hh + 0..7
@@ -259,8 +268,18 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   auto soft_a = [&](auto ec, auto rpc, bool masked, int key0) __attribute__((always_inline)) {
     constexpr int e = decltype(ec)::value, rp = decltype(rpc)::value;
     constexpr int nq = e / 16, s = e % 16;
-    if (masked)  // key0: this lane's first key of the chunk
-      sacc[rp][nq][s] += legal32(g, q_first + nq * 32 + l32, key0 + 8 * (s >> 2) + (s & 3)) ? 0.f : -INFINITY;
+    if (masked) {  // key0: this lane's first key of the chunk
+      // the window rule with the distance taken once per chunk and query tile
+      // (kept opaque, so the compiler does not precompute a distance per slot)
+      constexpr int cs = 8 * (s >> 2) + (s & 3);
+      const int qq = q_first + nq * 32 + l32;
+      int dq = qq + g.off - key0;
+      asm("" : "+v"(dq));
+      const int d = dq - cs, kk = key0 + cs;
+      const bool ok = (qq < g.n_q) & (kk < g.n_k) & (d >= 0) &
+                      ((d < g.w_near) | (kk < g.w_sink) | ((d >= g.lo) & (d < g.hi)));
+      sacc[rp][nq][s] += ok ? 0.f : -INFINITY;
+    }
     pv[e] = __builtin_amdgcn_exp2f(fmaf(sacc[rp][nq][s], c, -mu[nq]));
   };
   // second half (odd e): running maximum, bf16 pair, row sum
@@ -277,9 +296,9 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   // the element steps that belong to slot `slot` of NS
   auto soft_slot = [&](auto slotc, auto nsc, auto rpc, auto psc, bool masked, int key0) __attribute__((always_inline)) {
     constexpr int slot = decltype(slotc)::value, NS = decltype(nsc)::value;
-    static_for<32>([&](auto ec) {
+    static_for<16 * NQT>([&](auto ec) {
       constexpr int e = decltype(ec)::value;
-      constexpr int sa = e * NS / 32;
+      constexpr int sa = e * NS / (16 * NQT);
       constexpr int sb = sa + 1 < NS ? sa + 1 : sa;
       if constexpr (sa == slot) soft_a(ec, rpc, masked, key0);
       if constexpr (sb == slot) soft_b(ec, rpc, psc);
@@ -298,10 +317,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   // back; with 128-key blocks, V of block t is needed from its third step on,
   // so it is copied in the middle of block t - 1, once V of block t - 2 is no
   // longer read.
-#ifndef FWD_PF
-#define FWD_PF 2
-#endif
-  constexpr int PF = FWD_PF, RING = PF + 2;
+  constexpr int PF = 2, RING = PF + 2;
   int k_prev = 0;  // first key of the previous block
   // One block.  FIRST: the row's first block (nothing before its first chunk).
   // MPREV / MCUR: the chunks exponentiated here from the previous / this block
@@ -344,7 +360,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
         // block t - 1 was issued: V of block t is in (its copies were issued
         // before this block's K copies), and once every wave's reads of V of
         // block t - 1 are done, the copy of block t + 1 may overwrite it
-        if constexpr (FOUR)
+        if constexpr (FULL)
           __builtin_amdgcn_s_waitcnt(vmcnt_only(PPW));
         else
           __builtin_amdgcn_s_waitcnt(0);
@@ -382,13 +398,13 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
       // a chunk step without O^T products (start of the row): its S^T results
       // are read early in the next step, so settle them here
       if constexpr (FIRST && OLD && gi == NG - 1) {
-        mfma_settle(sacc[j & 1][0], sacc[j & 1][1]);
+        mfma_settle(sacc[j & 1]);
         __builtin_amdgcn_sched_barrier(0);
       }
     });
     // the last S^T products may still be in flight: wait states before
     // anything reads them
-    mfma_settle(sacc[1][0], sacc[1][1]);
+    mfma_settle(sacc[1]);
     __builtin_amdgcn_sched_barrier(0);
     // register placement: O^T accumulators and Q^T fragments in AGPRs (read
     // directly by the matrix cores), S^T and P^T in VGPRs; these emit nothing
@@ -403,7 +419,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
     k_prev = k_first;
     // the next block's K has landed (with 128-key blocks the next V may still
     // be in flight)
-    if constexpr (NCH == 4 && FOUR)
+    if constexpr (NCH == 4 && FULL)
       __builtin_amdgcn_s_waitcnt(vmcnt_only(PPW));
     else
       __builtin_amdgcn_s_waitcnt(0);
@@ -413,9 +429,9 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   // of its last two chunks
   auto drain = [&](int t) __attribute__((always_inline)) {
     using R1 = std::integral_constant<int, 1>;
-    static_for<32>([&](auto ec) { soft_a(ec, R1{}, true, k_prev + (NCH - 1) * 32 + 4 * hh); });
-    static_for<32>([&](auto ec) { soft_b(ec, R1{}, R1{}); });
-    if constexpr (NCH == 4 && FOUR) __builtin_amdgcn_s_waitcnt(0);  // (the repeated V copy of the mid-block)
+    static_for<16 * NQT>([&](auto ec) { soft_a(ec, R1{}, true, k_prev + (NCH - 1) * 32 + 4 * hh); });
+    static_for<16 * NQT>([&](auto ec) { soft_b(ec, R1{}, R1{}); });
+    if constexpr (NCH == 4 && FULL) __builtin_amdgcn_s_waitcnt(0);  // (the repeated V copy of the mid-block)
     const unsigned char* Vt = smem + vbuf_off(t);
     static_for<2 * 2 * MD>([&](auto gc) {
       constexpr int GG = decltype(gc)::value, jj = GG / (2 * MD), kk = (GG / MD) % 2, md = GG % MD;
@@ -469,7 +485,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
 #pragma unroll
         for (int nq = 0; nq < NQT; ++nq)
           sacc[0][nq] = ks == 0 ? mfma32_v0(a, qf[nq][0]) : mfma32_v(a, qf[nq][ks], sacc[0][nq]);
-        mfma_settle(sacc[0][0], sacc[0][1]);  // the next k-step reads these accumulators
+        mfma_settle(sacc[0]);  // the next k-step reads these accumulators
       }
 #pragma unroll
       for (int nq = 0; nq < NQT; ++nq) {
@@ -526,11 +542,11 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   }
 }
 
-template <int D, int BQ, int BK, bool FOUR>
+template <int D, int BQ, int BK, bool FULL>
 hipError_t launch_waves(const cowa_params& p, const SchedView& sv, int hpw, int n_hgroups, int waves, const void* q,
                         const void* k, const void* v, void* o, float* lse, hipStream_t stream) {
   using C = FwdCfg<D, BQ, BK>;
-  auto kern = fwd_bf16_kernel<D, BQ, BK, FOUR>;
+  auto kern = fwd_bf16_kernel<D, BQ, BK, FULL>;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -551,11 +567,11 @@ hipError_t launch_cfg(const cowa_params& p, const SchedView& sv, const void* q, 
   using C = FwdCfg<D, BQ, BK>;
   if (sv.n_kt > C::max_kblocks()) return hipErrorInvalidValue;
   const int G = p.h_q / p.h_k;
-  int hpw = 256 / BQ;  // QO heads per workgroup: up to 256 query rows (four waves)
+  int hpw = 256 / BQ;  // QO heads per workgroup: up to 256 query rows
   while (hpw > 1 && G % hpw != 0) hpw >>= 1;
   const int n_hgroups = p.h_q / hpw;
   const int waves = hpw * C::WPH;
-  if (waves == 4) return launch_waves<D, BQ, BK, true>(p, sv, hpw, n_hgroups, waves, q, k, v, o, lse, stream);
+  if (waves == C::NWF) return launch_waves<D, BQ, BK, true>(p, sv, hpw, n_hgroups, waves, q, k, v, o, lse, stream);
   return launch_waves<D, BQ, BK, false>(p, sv, hpw, n_hgroups, waves, q, k, v, o, lse, stream);
 }
 
