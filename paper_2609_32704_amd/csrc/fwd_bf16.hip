@@ -3,25 +3,27 @@
 // Work decomposition.  One workgroup per (QO block i, group of HPW QO heads
 // that share one KV head, sequence b): every QO head of a GQA group has the
 // same block set J_{h_k}(i), so the heads of a workgroup share each K/V block
-// staged in LDS.  Each 64-lane wave owns NQW query rows of one head (up to
-// 256 rows and 8 waves per workgroup).
+// staged in LDS.  Each 64-lane wave owns 64 query rows of one head (up to 256
+// rows, four waves, per workgroup).  Workgroups are grouped per XCD so that
+// rows sharing K/V blocks run together on one L2 (cluster_item).
 //
-// Per KV block j of J_{h_k}(i), visited in the schedule's descending order:
-//   * K_j and V_j are copied global -> LDS with direct 16-byte loads
-//     (global_load_lds), double buffered: block e+1 is in flight while block e
-//     is computed.  Rows are stored unpadded with their 16-byte chunks XOR
-//     swizzled by row, so both the row reads of K and the transposed reads of
-//     V hit distinct banks.
-//   * S^T = K_j Q^T on v_mfma_f32_16x16x32_bf16 (fp32 accumulate); Q^T stays
-//     in registers for the whole block.  Computing the transpose puts one
-//     query per lane column, which is the B-operand layout of the second
-//     product, so P never leaves registers.
+// Per KV block j of J_{h_k}(i), full blocks first, then partial ones:
+//   * K_j and V_j are copied global -> LDS with direct 16-byte buffer loads,
+//     double buffered and issued a block (K) or half a block (V) ahead.  Rows
+//     are stored unpadded with their 16-byte chunks XOR swizzled by row, so the
+//     row reads of K and the transposing reads of V hit distinct banks.
+//   * S^T = K_j Q^T on v_mfma_f32_32x32x16_bf16 (fp32 accumulate); Q^T stays in
+//     registers for the whole row.  The accumulator layout of S^T is the
+//     B-operand layout of P^T for O^T += V^T P^T, so P never leaves registers;
+//     the V^T fragments come from the row-major V_j through the transposing
+//     LDS read (ds_read_b64_tr_b16).
 //   * only blocks flagged partial evaluate the element mask of Eq. fwa_support;
-//   * online softmax in registers, base 2, with scale * log2(e) folded into one
-//     fused multiply-add per score; the O accumulator is rescaled only when a
-//     running maximum moved;
-//   * O^T += V_j^T P^T; the V^T fragments come straight from the row-major
-//     V_j in LDS through the transposing LDS read (ds_read_b64_tr_b16).
+//   * softmax in base 2 with a per-row fixed exponent offset (see below), the
+//     scale * log2(e) folded into one fused multiply-add per score, and the
+//     row sum l accumulated from the rounded bf16 P that enters O;
+//   * the 32-key chunks of a row form a software pipeline: S^T of chunk n and
+//     O^T of chunk n - 2 on the matrix cores while the vector ALUs exponentiate
+//     chunk n - 1.
 // Finally O = O / l and LSE = (m + log2 l) ln 2 (natural log).
 #include "internal.h"
 #include "window_rule.h"

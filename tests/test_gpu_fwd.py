@@ -113,3 +113,30 @@ def test_fwd_deterministic():
     o1, l1 = _run_fwd(w, t, dev)
     o2, l2 = _run_fwd(w, t, dev)
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_fwd_wide_score_range():
+    """Keys of the second 128-key block score far above the rest (about 90 in
+    log2 units), so rows whose first processed block is another one exceed the
+    forward's fixed exponent offset by more than its limit and run a second
+    pass with the row maximum; the fp64 oracle has no such limit."""
+    dev = need_gpu()
+    import paper_2609_32704_amd as cowa
+    n, h_q, h_k, d = 512, 2, 1, 64
+    rng = np.random.default_rng(11)
+    qf = (rng.standard_normal((1, h_q, n, d)) * 0.25 + 2.0).astype(np.float32)
+    kf = (rng.standard_normal((1, h_k, n, d)) * 0.1).astype(np.float32)
+    kf[:, :, 128:256, :] += 4.0
+    vf = rng.standard_normal((1, h_k, n, d)).astype(np.float32)
+    bits = [inputs.f32_to_bf16_bits(x) for x in (qf, kf, vf)]
+    vals = [inputs.bf16_bits_to_f64(b) for b in bits]
+    q, k, v = (to_dev(b, dev) for b in bits)
+    scale = d ** -0.5
+    o = torch.full_like(q, float("nan"))
+    lse = torch.full((1, h_q, n), float("nan"), dtype=torch.float32, device=dev)
+    cowa.fwd(q, k, v, 16, 512, 128, 128, scale, out=o, lse=lse)
+    torch.cuda.synchronize()
+    o_r, l_r = ref.forward(vals[0], vals[1], vals[2], 16, 512, scale)
+    assert l_r.max() > 60.0  # the range that needs the second pass
+    compare("O", to_host(o), o_r)
+    compare("LSE", to_host(lse), l_r)
