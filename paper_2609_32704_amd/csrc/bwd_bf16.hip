@@ -167,23 +167,45 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
   // compiler does not track (dma16/dma4): the Q and dO tiles, and the LSE and
   // D values of its 64 rows (waves 0 and 2 copy the LSE, 1 and 3 the D values,
   // the same data twice).  Each wave issues LOADS_PER_STEP copies per step and
-  // waits for them two steps later.  Rows past n_q repeat row n_q - 1; they
-  // occur in partial blocks only, where the mask gives them P = 0.  A cursor
+  // waits for them two steps later.  Rows past n_q (partial blocks only, where
+  // the mask gives them P = 0) hold zeros or an earlier step's rows.  A cursor
   // past the last step stages a copy of the last head's rows, never read.
   const uint32_t smem_base = lds_addr(smem);
+  // Each lane copies the same 16-byte column of its row in every 1 KB piece it
+  // takes: its byte offsets within a tile are fixed, and the tile position
+  // goes into the (scalar) buffer resource, whose size bounds the reads to the
+  // sequence (rows past n_q read as zero).
+  constexpr int RPL = 1024 / (D * 2);     // rows per 1 KB piece
+  constexpr int PPW = C::QT::LOADS / NW;  // pieces per wave and tile
+  uint32_t tile_off[PPW];
+  {
+    const int row0 = wave * RPL + lane / C::QT::CH;
+    const int col = (lane % C::QT::CH) ^ swz<C::QT::CH>(row0);
+#pragma unroll
+    for (int n = 0; n < PPW; ++n) tile_off[n] = (uint32_t)(((n * NW * RPL + row0) * D + col * 8) * 2);
+  }
   auto stage = [&](uint32_t ent, int hh, int sub, int slot) {
     hh = hh < G ? hh : G - 1;
     const int q0 = (int)(ent >> 1) * p.tile_q + sub * C::BQ;
     const int64_t row_base = ((int64_t)b * p.h_q + hk * G + hh) * p.n_q;
-    load_tile_asm<D, C::BQ, NW>(q + row_base * D, q0, p.n_q, smem_base + C::q_off(slot), wave, lane);
-    load_tile_asm<D, C::BQ, NW>(d_o + row_base * D, q0, p.n_q, smem_base + C::do_off(slot), wave, lane);
+    const uint32_t bytes = (uint32_t)(p.n_q - q0) * D * 2;
+    const i32x4 rq = buffer_rsrc(q + (row_base + q0) * D, bytes);
+    const i32x4 ro = buffer_rsrc(d_o + (row_base + q0) * D, bytes);
+#pragma unroll
+    for (int n = 0; n < PPW; ++n) {
+      dma16_buf(tile_off[n], rq, smem_base + C::q_off(slot) + (n * NW + wave) * 1024);
+      dma16_buf(tile_off[n], ro, smem_base + C::do_off(slot) + (n * NW + wave) * 1024);
+    }
     const int r = q0 + lane;
     const int rc = r < p.n_q ? r : p.n_q - 1;
     dma4(((wave & 1) ? dsum : lse) + row_base + rc,
          __builtin_amdgcn_readfirstlane(smem_base + C::rv_off(slot) + (wave & 1) * C::BQ * 4));
   };
 
-  __syncthreads();  // the entry lists are in LDS
+  // rows past the end of the sequence are not copied: give them finite values
+  for (int x = tid; x < 2 * C::NST * C::QT::BYTES / 16; x += blockDim.x)
+    reinterpret_cast<uint4*>(smem)[x] = uint4{0u, 0u, 0u, 0u};
+  __syncthreads();  // the entry lists and the zeroed stages are in LDS
   // prologue: steps 0 and 1 in flight
   if (n_steps > 0) {
     stage(entry_of(n2_ph, n2_k), n2_hh, n2_sub, 0);  // step 0

@@ -35,7 +35,6 @@ namespace {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 // S^T = K Q^T products with the accumulator in VGPRs (read by the softmax on the
 // vector ALUs) while O^T accumulates in AGPRs: written as assembly because the
@@ -81,21 +80,6 @@ __device__ inline float max3(float a, float b, float c) {
   float d;
   asm("v_max3_f32 %0, %1, %2, %3" : "=v"(d) : "v"(a), "v"(b), "v"(c));
   return d;
-}
-
-// Raw buffer resource over [base, base + bytes) (GFX9 layout, stride 0): loads
-// at offsets past `bytes` return zero instead of touching memory.
-__device__ inline i32x4 buffer_rsrc(const void* base, uint32_t bytes) {
-  const uint64_t a = (uint64_t)base;
-  return i32x4{(int)(uint32_t)a, (int)((a >> 32) & 0xffffu), (int)bytes, 0x00020000};
-}
-// 16 bytes per lane from a buffer straight into LDS: lane l lands at
-// lds_base + 16 l.  Issued as assembly and waited for explicitly, like dma16.
-__device__ inline void dma16_buf(uint32_t voff, i32x4 rsrc, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
-               :
-               : "v"(voff), "s"(rsrc), "s"(lds_base)
-               : "memory", "m0");
 }
 
 template <int D, int BQ, int BK>

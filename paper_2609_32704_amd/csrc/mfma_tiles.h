@@ -149,6 +149,23 @@ __device__ inline void dma4(const void* gptr, uint32_t lds_base) {
                : "memory", "m0");
 }
 
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Raw buffer resource over [base, base + bytes) (GFX9 layout, stride 0): loads
+// at offsets past `bytes` return zero instead of touching memory.
+__device__ inline i32x4 buffer_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)base;
+  return i32x4{(int)(uint32_t)a, (int)((a >> 32) & 0xffffu), (int)bytes, 0x00020000};
+}
+// 16 bytes per lane from a buffer straight into LDS: lane l lands at
+// lds_base + 16 l.  Issued as assembly and waited for explicitly, like dma16.
+__device__ inline void dma16_buf(uint32_t voff, i32x4 rsrc, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+               :
+               : "v"(voff), "s"(rsrc), "s"(lds_base)
+               : "memory", "m0");
+}
+
 // load_tile through dma16 (same layout and piece order).
 template <int D, int ROWS, int NW>
 __device__ inline void load_tile_asm(const __bf16* base, int first, int n_rows, uint32_t lds, int wave, int lane) {
