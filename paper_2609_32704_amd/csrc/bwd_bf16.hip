@@ -105,7 +105,6 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
   const Geo32 g = geo32(make_geo(p.n_q, p.n_k, p.w_sink, p.w_near, p.tile_q, BK, p.h_k_offset + hk, p.h_k_total));
 
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
-  const int nw = blockDim.x >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int64_t k_first = (int64_t)j * BK;
   const __bf16* kbase = k + ((int64_t)b * p.h_k + hk) * p.n_k * D;
@@ -462,7 +461,6 @@ struct DqCfg {
   static constexpr int NQW = NQW_;          // query rows per wave
   static constexpr int NTQ = NQW / 16;      // query tiles per wave
   static constexpr int BKC = 32;            // keys per chunk (one k-step of dQ^T += K^T dS^T)
-  static constexpr int MTK = 1;             // S^T and dP^T are computed 16 keys (one key tile) at a time
   static constexpr int NCH = BK / BKC;      // chunks per block
   static constexpr int KSD = D / 32;        // k-steps over d
   static constexpr int MTD = D / 16;        // d tiles of dQ^T
@@ -475,14 +473,14 @@ struct DqCfg {
 };
 
 template <int D, int BQ, int BK, int NQW>
-__global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, SchedView sv, int hpw, int n_hgroups,
+__global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, SchedView sv, int hpw,
                                                      const __bf16* __restrict__ q, const __bf16* __restrict__ k,
                                                      const __bf16* __restrict__ v, const __bf16* __restrict__ d_o,
                                                      const float* __restrict__ lse, const float* __restrict__ dsum,
                                                      __bf16* __restrict__ dq) {
   using C = DqCfg<D, BQ, BK, NQW>;
   using T = typename C::T;
-  constexpr int NTQ = C::NTQ, MTK = C::MTK, KSD = C::KSD, MTD = C::MTD;
+  constexpr int NTQ = C::NTQ, KSD = C::KSD, MTD = C::MTD;
   extern __shared__ __align__(1024) unsigned char smem[];
 
   const int nw = blockDim.x >> 6;
@@ -582,21 +580,6 @@ __global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, S
   f32x4 sacc[NTQ], pacc[NTQ];  // S^T, dP^T of 16 keys: rows keys 4 lg + rr, column query 16 nt + lr
   bf16x8 sb[2][NTQ];           // dS^T of the current and the previous chunk as B operands
 
-  // phase A: S^T and dP^T of key tile kt (keys 16 kt .. 16 kt + 15 of the block)
-  auto phase_a = [&](const unsigned char* Kt, const unsigned char* Vt, int kt) {
-#pragma unroll
-    for (int ks = 0; ks < KSD; ++ks) {
-      const int rowoff = kt * 16 * D * 2;
-      const bf16x8 ak = ld_row8(Kt + offr[ks] + rowoff);
-      const bf16x8 av = ld_row8(Vt + offr[ks] + rowoff);
-#pragma unroll
-      for (int nt = 0; nt < NTQ; ++nt) {
-        sacc[nt] = mfma16(ak, qf[nt][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sacc[nt]);
-        pacc[nt] = mfma16(av, gf[nt][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : pacc[nt]);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  };
   // dS^T of key tile kt, query tile nt into sb[sl], k-slots 4 (kt % 2) + rr
   // (key 16 kt + 4 lg + rr of the block); the chunk's k-slot order is the one
   // the transposing K^T read produces
@@ -610,13 +593,6 @@ __global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, S
       sb[sl][nt][4 * (kt & 1) + rr] = (__bf16)(pv * (pacc[nt][rr] - dd[nt]));
     }
   };
-  // dQ^T += K^T dS^T for chunk kc (from sb[sl]), d tile md
-  auto dq_mfma = [&](const unsigned char* Kt, int kc, int sl, int md) {
-    const bf16x8 a = ld_tr8(Kt + offt[md] + kc * C::BKC * D * 2, D * 2);
-#pragma unroll
-    for (int nt = 0; nt < NTQ; ++nt) qacc[md][nt] = mfma16(a, sb[sl][nt], qacc[md][nt]);
-  };
-
   // A block is a fixed sequence of groups, each an LDS read (issued PD groups
   // ahead) and the MFMAs that consume it:
   //   per key tile kt (16 keys): KSD groups of S^T/dP^T, then MTD/2 groups of
@@ -733,7 +709,7 @@ hipError_t launch_dq(const cowa_params& p, const SchedView& sv, const void* q, c
   const int n_hgroups = p.h_q / hpw;
   const int waves = hpw * C::WPH;
   const unsigned blocks = (unsigned)sv.n_qt * n_hgroups * p.batch;
-  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * waves), C::lds_bytes(sv.n_kt), stream, p, sv, hpw, n_hgroups,
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * waves), C::lds_bytes(sv.n_kt), stream, p, sv, hpw,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), static_cast<const __bf16*>(v),
                      static_cast<const __bf16*>(d_o), lse, dsum, static_cast<__bf16*>(dq));
   return hipGetLastError();

@@ -37,15 +37,6 @@ struct DecArgs {
   float c;  // softmax_scale * log2(e)
 };
 
-__device__ inline void bf16x8_to_f32(const uint4& w, float* f) {
-  const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    f[2 * t] = __uint_as_float(ws[t] << 16);
-    f[2 * t + 1] = __uint_as_float(ws[t] & 0xffff0000u);
-  }
-}
-
 // Sum over the DC lanes of each lane group (DC = 8 or 16 consecutive lanes,
 // inside one 16-lane DPP row), the result in every lane of the group:
 // quad butterflies, then mirrors within 8 and within 16 lanes.

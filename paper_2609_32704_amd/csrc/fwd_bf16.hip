@@ -65,14 +65,7 @@ __device__ inline f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& 
 __device__ inline void mfma_settle(f32x16& a, f32x16& b) {
   asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(a), "+v"(b));
 }
-__device__ inline void mfma_settle(f32x16& a) { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(a)); }
-template <int N>
-__device__ inline void mfma_settle(f32x16 (&r)[N]) {
-  if constexpr (N == 1)
-    mfma_settle(r[0]);
-  else
-    mfma_settle(r[0], r[1]);
-}
+__device__ inline void mfma_settle(f32x16 (&r)[2]) { mfma_settle(r[0], r[1]); }
 
 // max(a, b, c) in one instruction (fmaxf would first quiet each operand that
 // the compiler cannot prove canonical: the products above are opaque to it)
@@ -104,7 +97,7 @@ struct FwdCfg {
 // FULL: launched with NWF waves (the fast copy path; a compile-time choice
 // keeps the block step free of branches)
 template <int D, int BQ, int BK, bool FULL>
-__global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView sv, int hpw, int n_hgroups,
+__global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView sv, int hpw,
                                                        const __bf16* __restrict__ q, const __bf16* __restrict__ k,
                                                        const __bf16* __restrict__ v, __bf16* __restrict__ o,
                                                        float* __restrict__ lse) {
@@ -541,7 +534,7 @@ hipError_t launch_waves(const cowa_params& p, const SchedView& sv, int hpw, int 
     attr_set = true;
   }
   const unsigned blocks = (unsigned)sv.n_qt * n_hgroups * p.batch;
-  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * waves), C::lds_bytes(sv.n_kt), stream, p, sv, hpw, n_hgroups,
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * waves), C::lds_bytes(sv.n_kt), stream, p, sv, hpw,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), static_cast<const __bf16*>(v),
                      static_cast<__bf16*>(o), lse);
   return hipGetLastError();

@@ -133,6 +133,10 @@ __device__ inline void load_tile(const __bf16* base, int first, int n_rows, unsi
 // in its own s_waitcnt arithmetic nor makes unrelated LDS reads wait for them;
 // the caller waits for them explicitly (s_waitcnt vmcnt) before their data is
 // read and before the LDS they target is reused.  lds_base must be uniform.
+// Each copy sets M0 (the LDS destination) itself.  The compiler warns that it
+// may not preserve a reserved register named as clobbered; for gfx950 it keeps
+// no value of its own in M0 in these kernels (every M0 write in their device
+// assembly comes from these statements), so nothing live is overwritten.
 __device__ inline uint32_t lds_addr(const unsigned char* p) {
   return (uint32_t)(uintptr_t)(lds_void*)p;
 }
