@@ -140,9 +140,9 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
   const int subs = p.tile_q / C::BQ;
   const int steps_full = G * n_full * subs, n_steps = G * n_ent * subs;
   // cursor (phase: 0 full / 1 partial, QO head, list index, sub-block)
-  int c_ph = n_full > 0 ? 0 : 1, c_hh = 0, c_k = 0, c_sub = 0;  // step being computed
-  int n1_ph = c_ph, n1_hh = 0, n1_k = 0, n1_sub = 0;            // the next step (staged)
-  int n2_ph = c_ph, n2_hh = 0, n2_k = 0, n2_sub = 0;            // the step after (being staged)
+  int c_ph = n_full > 0 ? 0 : 1, c_k = 0, c_sub = 0;  // step being computed
+  int n1_ph = c_ph, n1_hh = 0, n1_k = 0, n1_sub = 0;  // the next step (staged)
+  int n2_ph = c_ph, n2_hh = 0, n2_k = 0, n2_sub = 0;  // the step after (being staged)
   auto advance = [&](int& ph, int& hh, int& kk, int& sub) {
     if (++sub == subs) {
       sub = 0;
@@ -183,22 +183,39 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
 #pragma unroll
     for (int n = 0; n < PPW; ++n) tile_off[n] = (uint32_t)(((n * NW * RPL + row0) * D + col * 8) * 2);
   }
-  auto stage = [&](uint32_t ent, int hh, int sub, int slot) {
+  // A step's copies are issued in pieces (piece n: 1 KB of Q and of dO per
+  // wave; and the row values), one piece every other product group early in
+  // the step two before it: issued back to back they hold the wave at the
+  // vector memory queue for hundreds of cycles.  (Spread over the whole step
+  // they would keep more scalar registers live than the kernel has.)
+  struct StageSrc {
+    int64_t off;       // byte offset of the step's first row in Q and in dO
+    uint32_t bytes;    // bytes from there to the end of the sequence
+    const float* rv;   // this lane's LSE or D value
+  };
+  auto stage_src = [&](uint32_t ent, int hh, int sub) -> StageSrc {
     hh = hh < G ? hh : G - 1;
     const int q0 = (int)(ent >> 1) * p.tile_q + sub * C::BQ;
     const int64_t row_base = ((int64_t)b * p.h_q + hk * G + hh) * p.n_q;
     const uint32_t bytes = (uint32_t)(p.n_q - q0) * D * 2;
-    const i32x4 rq = buffer_rsrc(q + (row_base + q0) * D, bytes);
-    const i32x4 ro = buffer_rsrc(d_o + (row_base + q0) * D, bytes);
-#pragma unroll
-    for (int n = 0; n < PPW; ++n) {
-      dma16_buf(tile_off[n], rq, smem_base + C::q_off(slot) + (n * NW + wave) * 1024);
-      dma16_buf(tile_off[n], ro, smem_base + C::do_off(slot) + (n * NW + wave) * 1024);
-    }
     const int r = q0 + lane;
     const int rc = r < p.n_q ? r : p.n_q - 1;
-    dma4(((wave & 1) ? dsum : lse) + row_base + rc,
-         __builtin_amdgcn_readfirstlane(smem_base + C::rv_off(slot) + (wave & 1) * C::BQ * 4));
+    return StageSrc{(row_base + q0) * D * 2, bytes, ((wave & 1) ? dsum : lse) + row_base + rc};
+  };
+  auto stage_piece = [&](const StageSrc& src, int n, int slot) {
+    const unsigned char* qb = reinterpret_cast<const unsigned char*>(q) + src.off;
+    const unsigned char* ob = reinterpret_cast<const unsigned char*>(d_o) + src.off;
+    dma16_buf(tile_off[n], buffer_rsrc(qb, src.bytes), smem_base + C::q_off(slot) + (n * NW + wave) * 1024);
+    dma16_buf(tile_off[n], buffer_rsrc(ob, src.bytes), smem_base + C::do_off(slot) + (n * NW + wave) * 1024);
+  };
+  auto stage_rows = [&](const StageSrc& src, int slot) {
+    dma4(src.rv, __builtin_amdgcn_readfirstlane(smem_base + C::rv_off(slot) + (wave & 1) * C::BQ * 4));
+  };
+  auto stage = [&](uint32_t ent, int hh, int sub, int slot) {
+    const StageSrc src = stage_src(ent, hh, sub);
+#pragma unroll
+    for (int n = 0; n < PPW; ++n) stage_piece(src, n, slot);
+    stage_rows(src, slot);
   };
 
   // rows past the end of the sequence are not copied: give them finite values
@@ -319,11 +336,12 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
     const unsigned char* dos = smem + C::do_off(slot);
     const float* rowv = reinterpret_cast<const float*>(smem + C::rv_off(slot));
     const int q0 = (int)(entry_of(c_ph, c_k) >> 1) * p.tile_q + c_sub * C::BQ;
-    stage(entry_of(n2_ph, n2_k), n2_hh, n2_sub, slot2);
+    const StageSrc src2 = stage_src(entry_of(n2_ph, n2_k), n2_hh, n2_sub);
 
     // groups 0 .. 4 NG - 1: S/dP(half 0), S/dP(half 1), dV/dK(half 0), dV/dK(half 1);
     // operand fragments are read PD groups ahead of their MFMAs
     constexpr int NGT = 4 * NG, PD = 1;
+    static_assert(2 * PPW <= NGT, "copy pieces per step");
     auto load_group = [&](int gg, bf16x8& fa, bf16x8& fb) {
       if (gg < NG)
         sdp_load(qs, dos, 0, gg, fa, fb);
@@ -342,6 +360,8 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
 #pragma unroll
     for (int gg = 0; gg < NGT; ++gg) {
       if (gg + PD < NGT) load_group(gg + PD, fa[(gg + PD) % (PD + 1)], fb[(gg + PD) % (PD + 1)]);
+      if (gg % 2 == 0 && gg < 2 * PPW) stage_piece(src2, gg / 2, slot2);
+      if (gg == 1) stage_rows(src2, slot2);
       // the row values of a half's first and second query tile are needed by
       // its softmax chunks [0, NG/2) and [NG/2, NG); each is loaded once the
       // previous half no longer reads that register
@@ -383,7 +403,7 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
     // flight), for every wave; and this step's slot is no longer read
     __builtin_amdgcn_s_waitcnt(vmcnt_only(C::LOADS_PER_STEP));
     __syncthreads();
-    c_ph = n1_ph, c_hh = n1_hh, c_k = n1_k, c_sub = n1_sub;
+    c_ph = n1_ph, c_k = n1_k, c_sub = n1_sub;
     n1_ph = n2_ph, n1_hh = n2_hh, n1_k = n2_k, n1_sub = n2_sub;
     advance(n2_ph, n2_hh, n2_k, n2_sub);
     slot = slot == 2 ? 0 : slot + 1;

@@ -183,6 +183,11 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
       load_tile_asm_nw<D, BK>(base, kf, p.n_k, smem_base + buf_off, wave, nw, lane);
     }
   };
+  // piece n of a block copy (full waves only), issued on its own
+  auto stage_piece = [&](const __bf16* base, int kf, int buf_off, int n) {
+    const i32x4 rs = buffer_rsrc(base + (int64_t)kf * D, (uint32_t)(p.n_k - kf) * D * 2);
+    dma16_buf(dma_off[n], rs, smem_base + buf_off + wave * 1024 + n * NWF * 1024);
+  };
   __syncthreads();  // the lists and the zeroed buffers are in LDS
 
   // Q^T fragments (B operands): query column 32 nq + l32, d = 16 ks + 8 hh + 0..7
@@ -305,7 +310,14 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
     constexpr bool FIRST = decltype(firstc)::value, MPREV = decltype(mprevc)::value;
     constexpr bool MCUR = decltype(mcurc)::value;
     const int k_first = (int)(entry_at(t) >> 1) * BK;
-    stage(kbase, t + 1, kbuf_off(t + 1));  // K buffer of block t - 1: free (the last block repeats itself)
+    // K of block t + 1 goes into the K buffer of block t - 1, which is free
+    // (the last block repeats itself).  With 128-key blocks and full waves the
+    // copies of K (from the block start) and of V (from the mid-block barrier)
+    // go out one 1 KB piece per product group: a burst of them would hold the
+    // wave at the vector memory queue.
+    constexpr bool SPREAD = FULL && NCH == 4;
+    [[maybe_unused]] const int kf_next = (int)(entry_at(t + 1) >> 1) * BK;
+    if constexpr (!SPREAD) stage(kbase, t + 1, kbuf_off(t + 1));
     if constexpr (NCH == 2) stage(vbase, t, vbuf_off(t));  // V buffer of block t - 2: free
     const unsigned char* Kt = smem + kbuf_off(t);
     const unsigned char* Vt = smem + vbuf_off(t);
@@ -344,9 +356,12 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
         else
           __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
-        stage(vbase, t + 1, vbuf_off(t + 1));
+        if constexpr (!SPREAD) stage(vbase, t + 1, vbuf_off(t + 1));
         __builtin_amdgcn_sched_barrier(0);
       }
+      if constexpr (SPREAD && GG < PPW) stage_piece(kbase, kf_next, kbuf_off(t + 1), GG);
+      if constexpr (SPREAD && GG >= 2 * NG - PF && GG < 2 * NG - PF + PPW)
+        stage_piece(vbase, kf_next, vbuf_off(t + 1), GG - (2 * NG - PF));
       if constexpr (GG + PF < NGS) load(std::integral_constant<int, GG + PF>{}, fa[(GG + PF) % RING]);
       const bf16x8& a = fa[GG % RING];
       static_for<NQT>([&](auto mc) {
