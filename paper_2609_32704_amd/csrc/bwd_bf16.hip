@@ -492,7 +492,9 @@ struct DqCfg {
   static int max_kblocks() { return (LDS_MAX - MAIN_BYTES) / 4; }
 };
 
-template <int D, int BQ, int BK, int NQW>
+// W4: the workgroup has exactly four waves (then the next block's copies are
+// spread over the block's product groups).
+template <int D, int BQ, int BK, int NQW, bool W4>
 __global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, SchedView sv, int hpw,
                                                      const __bf16* __restrict__ q, const __bf16* __restrict__ k,
                                                      const __bf16* __restrict__ v, const __bf16* __restrict__ d_o,
@@ -557,6 +559,20 @@ __global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, S
   };
   __syncthreads();  // the lists are in LDS
   if (n_ent > 0) stage(entry_at(0), 0);
+  // With four waves, the next block's K and V copies go out one 1 KB piece per
+  // product group (K piece n, then V piece n) instead of a burst that would
+  // hold the wave at the vector memory queue; past the last block the last
+  // block is copied again (into the free buffer, never read).
+  constexpr int RPL = 1024 / (D * 2), PPW4 = T::LOADS / 4;
+  static_assert(!W4 || (T::LOADS % 4 == 0 && (4 * RPL) % 16 == 0), "piece layout");
+  const int row0 = wave * RPL + lane / T::CH;
+  const int col0 = ((lane % T::CH) ^ swz<T::CH>(row0)) << 3;
+  auto stage_piece = [&](const __bf16* base, int kf, int buf, int n, int isv) {
+    int r = kf + n * 4 * RPL + row0;
+    r = r < p.n_k ? r : p.n_k - 1;
+    dma16(base + (int64_t)r * D + col0,
+          __builtin_amdgcn_readfirstlane(smem_base + buf * 2 * T::BYTES + isv * T::BYTES + (n * 4 + wave) * 1024));
+  };
 
   // Q^T and dO^T fragments (B operands): query column nt*16 + lr, d = ks*32 + 8*lg + 0..7;
   // per-query LSE (base 2; a row without keys or past n_q gets +inf, so P = 0) and D
@@ -619,6 +635,7 @@ __global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, S
   //   dQ^T for the previous 32-key chunk interleaved with dS^T of tile kt;
   //   finally MTD groups of dQ^T for the last chunk.
   constexpr int GPS = KSD + MTD / 2, NKT = 2 * C::NCH, NGB = NKT * GPS + MTD, PD = 1;
+  static_assert(!W4 || 2 * PPW4 <= NGB, "copy pieces per block");
   auto load_g = [&](const unsigned char* Kt, const unsigned char* Vt, int gg, bf16x8& fa, bf16x8& fb) {
     if (gg < NKT * GPS) {
       const int kt = gg / GPS, r = gg % GPS;
@@ -665,7 +682,10 @@ __global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, S
     const int buf = t & 1;
     const uint32_t ent = entry_at(t);
     const int k_first = (int)(ent >> 1) * BK;
-    if (t + 1 < n_ent) stage(entry_at(t + 1), buf ^ 1);  // prefetch the next block
+    [[maybe_unused]] const int kf_next = (int)(entry_at(t + 1) >> 1) * BK;
+    if constexpr (!W4) {
+      if (t + 1 < n_ent) stage(entry_at(t + 1), buf ^ 1);  // prefetch the next block
+    }
     const unsigned char* Kt = smem + buf * 2 * T::BYTES;
     const unsigned char* Vt = Kt + T::BYTES;
     bf16x8 fa[PD + 1], fb[PD + 1];
@@ -673,6 +693,7 @@ __global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, S
     __builtin_amdgcn_sched_barrier(0);
     static_for<NGB>([&](auto ic) {
       constexpr int gg = decltype(ic)::value;
+      if constexpr (W4 && gg < 2 * PPW4) stage_piece((gg & 1) ? vbase : kbase, kf_next, buf ^ 1, gg >> 1, gg & 1);
       if constexpr (gg + PD < NGB) load_g(Kt, Vt, gg + PD, fa[(gg + PD) % (PD + 1)], fb[(gg + PD) % (PD + 1)]);
       exec_g(gg, fa[gg % (PD + 1)], fb[gg % (PD + 1)], masked, k_first);
       __builtin_amdgcn_sched_barrier(0);
@@ -710,12 +731,12 @@ __global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, S
   }
 }
 
-template <int D, int BQ, int BK, int NQW = 64>
-hipError_t launch_dq(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
-                     const void* d_o, const float* lse, const float* dsum, void* dq, hipStream_t stream) {
+template <int D, int BQ, int BK, int NQW, bool W4>
+hipError_t launch_dq_w(const cowa_params& p, const SchedView& sv, int hpw, int waves, const void* q, const void* k,
+                       const void* v, const void* d_o, const float* lse, const float* dsum, void* dq,
+                       hipStream_t stream) {
   using C = DqCfg<D, BQ, BK, NQW>;
-  if (sv.n_kt > C::max_kblocks()) return hipErrorInvalidValue;
-  auto kern = bwd_dq_kernel<D, BQ, BK, NQW>;
+  auto kern = bwd_dq_kernel<D, BQ, BK, NQW, W4>;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -723,16 +744,25 @@ hipError_t launch_dq(const cowa_params& p, const SchedView& sv, const void* q, c
     if (err != hipSuccess) return err;
     attr_set = true;
   }
-  const int G = p.h_q / p.h_k;
-  int hpw = 256 / BQ;  // up to 256 query rows per workgroup
-  while (hpw > 1 && G % hpw != 0) hpw >>= 1;
   const int n_hgroups = p.h_q / hpw;
-  const int waves = hpw * C::WPH;
   const unsigned blocks = (unsigned)sv.n_qt * n_hgroups * p.batch;
   hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * waves), C::lds_bytes(sv.n_kt), stream, p, sv, hpw,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), static_cast<const __bf16*>(v),
                      static_cast<const __bf16*>(d_o), lse, dsum, static_cast<__bf16*>(dq));
   return hipGetLastError();
+}
+
+template <int D, int BQ, int BK, int NQW = 64>
+hipError_t launch_dq(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
+                     const void* d_o, const float* lse, const float* dsum, void* dq, hipStream_t stream) {
+  using C = DqCfg<D, BQ, BK, NQW>;
+  if (sv.n_kt > C::max_kblocks()) return hipErrorInvalidValue;
+  const int G = p.h_q / p.h_k;
+  int hpw = 256 / BQ;  // up to 256 query rows per workgroup
+  while (hpw > 1 && G % hpw != 0) hpw >>= 1;
+  const int waves = hpw * C::WPH;
+  if (waves == 4) return launch_dq_w<D, BQ, BK, NQW, true>(p, sv, hpw, waves, q, k, v, d_o, lse, dsum, dq, stream);
+  return launch_dq_w<D, BQ, BK, NQW, false>(p, sv, hpw, waves, q, k, v, d_o, lse, dsum, dq, stream);
 }
 
 }  // namespace
