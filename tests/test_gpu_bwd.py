@@ -77,6 +77,9 @@ ODD = [
     ("wide_windows", 1, 500, 500, 2, 2, 64, 400, 400, 64, 128, 0, 0),
     ("no_near", 1, 300, 300, 2, 2, 64, 0, 0, 64, 64, 0, 0),
     ("tiny", 1, 5, 9, 2, 1, 128, 1, 2, 64, 64, 0, 0),
+    # four-wave dQ workgroups of 64-row query blocks (4 QO heads each)
+    ("gqa4_tq64", 1, 900, 900, 8, 2, 128, 8, 200, 64, 128, 0, 0),
+    ("gqa4_d64_t64", 1, 650, 650, 4, 1, 64, 16, 130, 64, 64, 0, 0),
 ]
 
 
