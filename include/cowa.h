@@ -197,7 +197,12 @@ cowa_status cowa_bwd_dq(const cowa_params* p, const cowa_schedule_t* s,
                         const float* lse, const void* d_o, void* dq,
                         void* workspace, size_t ws_bytes, void* stream);
 
-/* Workspace bytes of one decoding step: split partial states (m, l, O). */
+/* Workspace bytes of one decoding step (Sec. 2.3, decoding execution): the
+ * visible keys of each (sequence, KV head) are split into ranges processed in
+ * parallel, and each range leaves a partial softmax state per QO head -- its
+ * running maximum m, its sum l and its unnormalised output O (float32) --
+ * that a second kernel merges.  Depends on batch, h_q, head_dim, n_max, the
+ * windows and split_keys. */
 cowa_status cowa_decode_workspace_size(const cowa_decode_params* p, size_t* bytes);
 
 /* One decoding step (Sec. 2.3): the forward with N_q = 1 for every sequence b,

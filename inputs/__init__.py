@@ -105,9 +105,10 @@ def normal_bf16(shape, seq):
     return bits, bf16_bits_to_f64(bits)
 
 
-def train_tensors(w, which=("q", "k", "v", "do"), key=None):
+def train_tensors(w, which=("q", "k", "v", "do"), key=None, values=True):
     """Inputs of a forward/backward workload.  Returns {name: (device_payload,
-    float64 values)} where the payload is uint16 bf16 bits or float32."""
+    float64 values)} where the payload is uint16 bf16 bits or float32
+    (values=False: the float64 values are None, which saves their memory)."""
     key = w.name if key is None else key
     shapes = {"q": (w.batch, w.h_q, w.n_q, w.head_dim), "k": (w.batch, w.h_k, w.n_k, w.head_dim),
               "v": (w.batch, w.h_k, w.n_k, w.head_dim), "do": (w.batch, w.h_q, w.n_q, w.head_dim)}
@@ -115,10 +116,13 @@ def train_tensors(w, which=("q", "k", "v", "do"), key=None):
     for name in which:
         seq = seed_sequence(key, name)
         if w.dtype == "bf16":
-            out[name] = normal_bf16(shapes[name], seq)
+            if values:
+                out[name] = normal_bf16(shapes[name], seq)
+            else:
+                out[name] = (f32_to_bf16_bits(normal(shapes[name], seq)), None)
         else:
             x = normal(shapes[name], seq)
-            out[name] = (x, x.astype(np.float64))
+            out[name] = (x, x.astype(np.float64) if values else None)
     return out
 
 

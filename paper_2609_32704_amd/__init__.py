@@ -13,6 +13,8 @@ the helpers below wrap them for torch tensors:
 * ``fwd``       -- cowa_fwd: O and LSE
 * ``bwd``       -- cowa_bwd: dQ, dK, dV
 * ``decode``    -- cowa_decode: one decoding step over a KV cache
+* ``attention`` -- differentiable attention (torch.autograd.Function over
+                   cowa_fwd and cowa_bwd)
 """
 
 import math
@@ -22,7 +24,7 @@ from ._abi import (CowaError, COWA_BF16, COWA_FP32, cowa_version, cowa_last_erro
                    cowa_schedule_size)
 
 __all__ = ["CowaError", "make_params", "make_decode_params", "Schedule", "fwd", "bwd", "decode", "windows",
-           "cowa_version"]
+           "attention", "cowa_version"]
 
 
 def _torch():
@@ -105,14 +107,42 @@ class Schedule:
                 "fwd_ent": view(s.off_fwd_ent, s.nnz), "bwd_ent": view(s.off_bwd_ent, s.nnz)}
 
 
-def _check(t, name, dtype, ndim):
+def _validate(specs):
+    """specs: (tensor, name, dtype, shape) per tensor; None tensors are skipped.
+    Raise ValueError unless every tensor is a contiguous torch tensor of its
+    dtype and exact shape (all of them checked first), and then unless all of
+    them are on the GPU of the first.  Every check runs before anything is
+    passed to the library, whose kernels index every buffer by the shapes
+    taken from q and k."""
     torch = _torch()
-    if not isinstance(t, torch.Tensor) or not t.is_cuda:
-        raise ValueError(f"{name} must be a device tensor")
-    if t.dtype != dtype:
-        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
-    if t.dim() != ndim or not t.is_contiguous():
-        raise ValueError(f"{name} must be a contiguous {ndim}-d tensor")
+    specs = [sp for sp in specs if sp[0] is not None]
+    for t, name, dtype, shape in specs:
+        if not isinstance(t, torch.Tensor):
+            raise ValueError(f"{name} must be a torch.Tensor")
+        if t.dtype != dtype:
+            raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+        if tuple(t.shape) != tuple(shape):
+            raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    dev = specs[0][0].device
+    for t, name, _, _ in specs:
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a device tensor")
+        if t.device != dev:
+            raise ValueError(f"{name} is on {t.device}, expected {dev}")
+
+
+def _dims(q, k, name_q="q", name_k="k"):
+    """(B, H_q, N_q, d, H_k, N_k) from q [B,H_q,N_q,d] and k [B,H_k,N_k,d]."""
+    torch = _torch()
+    for t, n in ((q, name_q), (k, name_k)):
+        if not isinstance(t, torch.Tensor) or t.dim() != 4:
+            raise ValueError(f"{n} must be a 4-d tensor [B, H, N, d]")
+    bsz, h_q, n_q, d = q.shape
+    if k.shape[0] != bsz or k.shape[3] != d:
+        raise ValueError(f"{name_k} has shape {tuple(k.shape)}; expected [B={bsz}, H_k, N_k, d={d}]")
+    return bsz, h_q, n_q, d, k.shape[1], k.shape[2]
 
 
 def fwd(q, k, v, w_sink, w_near, tile_q, tile_k, softmax_scale=None, h_k_total=None, h_k_offset=0, schedule=None,
@@ -120,13 +150,10 @@ def fwd(q, k, v, w_sink, w_near, tile_q, tile_k, softmax_scale=None, h_k_total=N
     """cowa_fwd.  q [B,H_q,N_q,d], k/v [B,H_k,N_k,d] (bf16 or fp32, contiguous).
     Returns (o, lse).  ``schedule`` may be a prebuilt Schedule for these shapes."""
     torch = _torch()
-    _check(q, "q", q.dtype, 4)
-    _check(k, "k", q.dtype, 4)
-    _check(v, "v", q.dtype, 4)
-    bsz, h_q, n_q, d = q.shape
-    h_k, n_k = k.shape[1], k.shape[2]
-    if k.shape != v.shape or k.shape[0] != bsz or k.shape[3] != d:
-        raise ValueError("k and v must be [B, H_k, N_k, d] matching q")
+    bsz, h_q, n_q, d, h_k, n_k = _dims(q, k)
+    _validate([(q, "q", q.dtype, (bsz, h_q, n_q, d)), (k, "k", q.dtype, (bsz, h_k, n_k, d)),
+               (v, "v", q.dtype, (bsz, h_k, n_k, d)), (out, "out", q.dtype, (bsz, h_q, n_q, d)),
+               (lse, "lse", torch.float32, (bsz, h_q, n_q))])
     p = make_params(bsz, n_q, n_k, h_q, h_k, d, w_sink, w_near, tile_q, tile_k, softmax_scale,
                     _dtype_code(q.dtype), h_k_total, h_k_offset)
     if schedule is None:
@@ -135,8 +162,6 @@ def fwd(q, k, v, w_sink, w_near, tile_q, tile_k, softmax_scale=None, h_k_total=N
         out = torch.empty_like(q)
     if lse is None:
         lse = torch.empty((bsz, h_q, n_q), dtype=torch.float32, device=q.device)
-    _check(out, "out", q.dtype, 4)
-    _check(lse, "lse", torch.float32, 3)
     _abi.cowa_fwd(p, schedule.s, q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
                   _stream(stream))
     return out, lse
@@ -146,26 +171,24 @@ def bwd(q, k, v, o, lse, do, w_sink, w_near, tile_q, tile_k, softmax_scale=None,
         schedule=None, workspace=None, dq=None, dk=None, dv=None, stream=None):
     """cowa_bwd.  Returns (dq, dk, dv) for bf16 inputs."""
     torch = _torch()
-    for t, n in ((q, "q"), (o, "o"), (do, "do")):
-        _check(t, n, q.dtype, 4)
-    _check(k, "k", q.dtype, 4)
-    _check(v, "v", q.dtype, 4)
-    _check(lse, "lse", torch.float32, 3)
-    bsz, h_q, n_q, d = q.shape
-    h_k, n_k = k.shape[1], k.shape[2]
+    bsz, h_q, n_q, d, h_k, n_k = _dims(q, k)
+    qs, ks = (bsz, h_q, n_q, d), (bsz, h_k, n_k, d)
+    _validate([(q, "q", q.dtype, qs), (k, "k", q.dtype, ks), (v, "v", q.dtype, ks), (o, "o", q.dtype, qs),
+               (do, "do", q.dtype, qs), (lse, "lse", torch.float32, (bsz, h_q, n_q)), (dq, "dq", q.dtype, qs),
+               (dk, "dk", q.dtype, ks), (dv, "dv", q.dtype, ks),
+               (workspace, "workspace", torch.uint8, (None if workspace is None else workspace.numel(),))])
     p = make_params(bsz, n_q, n_k, h_q, h_k, d, w_sink, w_near, tile_q, tile_k, softmax_scale,
                     _dtype_code(q.dtype), h_k_total, h_k_offset)
+    need = _abi.cowa_bwd_workspace_size(p)
+    if workspace is not None and workspace.numel() < need:
+        raise ValueError(f"workspace has {workspace.numel()} bytes, the backward needs {need}")
     if schedule is None:
         schedule = Schedule(p, q.device, stream)
-    need = _abi.cowa_bwd_workspace_size(p)
     if workspace is None:
         workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=q.device)
     dq = torch.empty_like(q) if dq is None else dq
     dk = torch.empty_like(k) if dk is None else dk
     dv = torch.empty_like(v) if dv is None else dv
-    _check(dq, "dq", q.dtype, 4)
-    _check(dk, "dk", q.dtype, 4)
-    _check(dv, "dv", q.dtype, 4)
     _abi.cowa_bwd(p, schedule.s, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
                   do.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), workspace.data_ptr(),
                   workspace.numel(), _stream(stream))
@@ -177,15 +200,22 @@ def decode(q, k_cache, v_cache, seqlens_k, w_sink, w_near, softmax_scale=None, h
     """cowa_decode.  q [B,H_q,d], caches [B,H_k,n_max,d] bf16, seqlens_k int32 [B]
     on the device.  Returns (o [B,H_q,d], lse [B,H_q])."""
     torch = _torch()
-    _check(q, "q", q.dtype, 3)
-    _check(k_cache, "k_cache", q.dtype, 4)
-    _check(v_cache, "v_cache", q.dtype, 4)
-    _check(seqlens_k, "seqlens_k", torch.int32, 1)
+    if not isinstance(q, torch.Tensor) or q.dim() != 3:
+        raise ValueError("q must be a 3-d tensor [B, H_q, d]")
+    if not isinstance(k_cache, torch.Tensor) or k_cache.dim() != 4:
+        raise ValueError("k_cache must be a 4-d tensor [B, H_k, n_max, d]")
     bsz, h_q, d = q.shape
     h_k, n_max = k_cache.shape[1], k_cache.shape[2]
+    cs = (bsz, h_k, n_max, d)
+    _validate([(q, "q", q.dtype, (bsz, h_q, d)), (k_cache, "k_cache", q.dtype, cs), (v_cache, "v_cache", q.dtype, cs),
+               (seqlens_k, "seqlens_k", torch.int32, (bsz,)), (out, "out", q.dtype, (bsz, h_q, d)),
+               (lse, "lse", torch.float32, (bsz, h_q)),
+               (workspace, "workspace", torch.uint8, (None if workspace is None else workspace.numel(),))])
     p = make_decode_params(bsz, h_q, h_k, d, n_max, w_sink, w_near, softmax_scale, h_k_total, h_k_offset,
                            split_keys, _dtype_code(q.dtype))
     need = _abi.cowa_decode_workspace_size(p)
+    if workspace is not None and workspace.numel() < need:
+        raise ValueError(f"workspace has {workspace.numel()} bytes, decoding needs {need}")
     if workspace is None:
         workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=q.device)
     if out is None:
@@ -195,3 +225,55 @@ def decode(q, k_cache, v_cache, seqlens_k, w_sink, w_near, softmax_scale=None, h
     _abi.cowa_decode(p, q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), seqlens_k.data_ptr(), out.data_ptr(),
                      lse.data_ptr(), workspace.data_ptr(), workspace.numel(), _stream(stream))
     return out, lse
+
+
+class _Attention:
+    """torch.autograd.Function around cowa_fwd / cowa_bwd (built lazily so that
+    importing the package does not import torch)."""
+    fn = None
+
+    @classmethod
+    def get(cls):
+        if cls.fn is None:
+            torch = _torch()
+
+            class CowaAttentionFn(torch.autograd.Function):
+                @staticmethod
+                def forward(ctx, q, k, v, w_sink, w_near, tile_q, tile_k, softmax_scale, h_k_total, h_k_offset):
+                    q, k, v = q.contiguous(), k.contiguous(), v.contiguous()
+                    p = make_params(q.shape[0], q.shape[2], k.shape[2], q.shape[1], k.shape[1], q.shape[3],
+                                    w_sink, w_near, tile_q, tile_k, softmax_scale, _dtype_code(q.dtype),
+                                    h_k_total, h_k_offset)
+                    sched = Schedule(p, q.device)
+                    o, lse = fwd(q, k, v, w_sink, w_near, tile_q, tile_k, softmax_scale, h_k_total, h_k_offset,
+                                 schedule=sched)
+                    ctx.save_for_backward(q, k, v, o, lse)
+                    ctx.mark_non_differentiable(lse)
+                    ctx.set_materialize_grads(False)
+                    ctx.cfg = (w_sink, w_near, tile_q, tile_k, softmax_scale, h_k_total, h_k_offset)
+                    ctx.sched = sched
+                    return o, lse
+
+                @staticmethod
+                def backward(ctx, d_o, d_lse):
+                    q, k, v, o, lse = ctx.saved_tensors
+                    if d_o is None:
+                        return (None,) * 10
+                    w_sink, w_near, tile_q, tile_k, scale, h_k_total, h_k_offset = ctx.cfg
+                    dq, dk, dv = bwd(q, k, v, o, lse, d_o.contiguous(), w_sink, w_near, tile_q, tile_k, scale,
+                                     h_k_total, h_k_offset, schedule=ctx.sched)
+                    return dq, dk, dv, None, None, None, None, None, None, None
+
+            cls.fn = CowaAttentionFn
+        return cls.fn
+
+
+def attention(q, k, v, w_sink, w_near, tile_q=128, tile_k=128, softmax_scale=None, h_k_total=None, h_k_offset=0,
+              return_lse=False):
+    """Differentiable CoWA attention (torch autograd): the forward runs cowa_fwd
+    and saves O and LSE; the backward runs cowa_bwd (deterministic: the same
+    inputs give bitwise the same gradients).  q [B,H_q,N_q,d], k/v
+    [B,H_k,N_k,d], bf16 for the backward.  Returns O (and LSE, treated as a
+    non-differentiable output, if return_lse)."""
+    o, lse = _Attention.get().apply(q, k, v, w_sink, w_near, tile_q, tile_k, softmax_scale, h_k_total, h_k_offset)
+    return (o, lse) if return_lse else o

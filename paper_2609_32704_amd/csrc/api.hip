@@ -3,10 +3,14 @@
 // writes nothing.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
+#include <set>
+#include <utility>
 
 #include "internal.h"
 #include "window_rule.h"
@@ -75,17 +79,16 @@ cowa_status check_device() {
     (void)hipGetLastError();
     return fail(COWA_ERR_NO_DEVICE, "no HIP device");
   }
-  static int ok_cache[64] = {0};  // 0 unknown, 1 ok, -1 not gfx950
-  if (dev < 64 && ok_cache[dev] != 0) {
-    return ok_cache[dev] > 0 ? COWA_OK : fail(COWA_ERR_NO_DEVICE, "device %d is not gfx950", dev);
-  }
+  static std::atomic<int> ok_cache[64];  // 0 unknown, 1 ok, -1 not gfx950 (zero-initialised statics)
+  const int known = dev < 64 ? ok_cache[dev].load(std::memory_order_acquire) : 0;
+  if (known != 0) return known > 0 ? COWA_OK : fail(COWA_ERR_NO_DEVICE, "device %d is not gfx950", dev);
   hipDeviceProp_t prop;
   if (hipGetDeviceProperties(&prop, dev) != hipSuccess) {
     (void)hipGetLastError();
     return fail(COWA_ERR_NO_DEVICE, "cannot query device %d", dev);
   }
   const bool ok = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
-  if (dev < 64) ok_cache[dev] = ok ? 1 : -1;
+  if (dev < 64) ok_cache[dev].store(ok ? 1 : -1, std::memory_order_release);
   return ok ? COWA_OK : fail(COWA_ERR_NO_DEVICE, "device %d is %s, the library is built for gfx950", dev, prop.gcnArchName);
 }
 
@@ -107,6 +110,23 @@ cowa_status check_tensor(const void* ptr, const char* name, size_t align) {
   } while (0)
 
 }  // namespace
+
+namespace cowa {
+
+hipError_t allow_lds(const void* kernel, int bytes) {
+  int dev = -1;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) return err;
+  static std::mutex mu;
+  static std::set<std::pair<const void*, int>> done;
+  std::lock_guard<std::mutex> lock(mu);
+  if (done.count({kernel, dev})) return hipSuccess;
+  err = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (err == hipSuccess) done.insert({kernel, dev});
+  return err;
+}
+
+}  // namespace cowa
 
 extern "C" {
 
@@ -234,7 +254,7 @@ cowa_status cowa_fwd(const cowa_params* p, const cowa_schedule_t* s, const void*
   if ((int64_t)s->n_qt * p->h_q * p->batch >= (int64_t(1) << 31))
     return fail(COWA_ERR_UNSUPPORTED, "too many query blocks for one launch");
   if (p->dtype == COWA_BF16 && !cowa::fwd_bf16_supported(p->head_dim, p->tile_q, p->tile_k))
-    return fail(COWA_ERR_UNSUPPORTED, "bf16 forward is built for tile_q in {64,128}, tile_k in {32,64,128}");
+    return fail(COWA_ERR_UNSUPPORTED, "bf16 forward is built for tile_q and tile_k in {64, 128} (got %d x %d)", p->tile_q, p->tile_k);
   if (p->dtype == COWA_BF16 && s->n_kt > cowa::fwd_bf16_max_kblocks(p->head_dim, p->tile_k))
     return fail(COWA_ERR_UNSUPPORTED, "bf16 forward supports at most %d key blocks (got %d)",
                 cowa::fwd_bf16_max_kblocks(p->head_dim, p->tile_k), s->n_kt);
@@ -256,7 +276,7 @@ cowa_status cowa_bwd_workspace_size(const cowa_params* p, size_t* bytes) {
   return COWA_OK;
 }
 
-// Common checks of the backward stages; the workspace holds D = rowsum(O * dO).
+// Checks shared by the backward stages; the workspace holds D = rowsum(O * dO).
 static cowa_status check_bwd(const cowa_params* p, size_t ws_bytes, void* workspace, float** dsum) {
   COWA_TRY(check_params(p));
   if (p->dtype != COWA_BF16) return fail(COWA_ERR_UNSUPPORTED, "backward is built for bf16 only");
@@ -272,12 +292,24 @@ static cowa_status check_bwd(const cowa_params* p, size_t ws_bytes, void* worksp
   if (n_kt > cowa::bwd_dq_max_kblocks(p->head_dim, p->tile_k))
     return fail(COWA_ERR_UNSUPPORTED, "backward supports at most %d key blocks (got %lld)",
                 cowa::bwd_dq_max_kblocks(p->head_dim, p->tile_k), (long long)n_kt);
+  // one workgroup per (KV block, KV head, sequence) in the dK/dV pass and per
+  // (QO block, QO head, sequence) at most in the dQ pass: grid limit 2^31
+  if (n_kt * p->h_k * p->batch >= (int64_t(1) << 31))
+    return fail(COWA_ERR_UNSUPPORTED, "too many key blocks for one launch");
+  if (n_qt * p->h_q * p->batch >= (int64_t(1) << 31))
+    return fail(COWA_ERR_UNSUPPORTED, "too many query blocks for one launch");
   size_t need = 0;
   COWA_TRY(cowa_bwd_workspace_size(p, &need));
   if (p->batch > 0 && (!workspace || ws_bytes < need || !aligned(workspace, 256)))
     return fail(COWA_ERR_WORKSPACE, "backward needs a 256-byte aligned workspace of %zu bytes (got %zu)", need, ws_bytes);
   *dsum = static_cast<float*>(workspace);
   return COWA_OK;
+}
+
+// Pointer checks of each stage (after check_bwd; batch > 0).
+static cowa_status check_prepare_ptrs(const void* o, const void* d_o) {
+  COWA_TRY(check_tensor(o, "o", 16));
+  return check_tensor(d_o, "d_o", 16);
 }
 
 static cowa_status check_qkv_lse_do(const void* q, const void* k, const void* v, const float* lse, const void* d_o) {
@@ -288,13 +320,25 @@ static cowa_status check_qkv_lse_do(const void* q, const void* k, const void* v,
   return check_tensor(d_o, "d_o", 16);
 }
 
+static cowa_status check_main_ptrs(const void* q, const void* k, const void* v, const float* lse, const void* d_o,
+                                   const void* dk, const void* dv) {
+  COWA_TRY(check_qkv_lse_do(q, k, v, lse, d_o));
+  COWA_TRY(check_tensor(dk, "dk", 16));
+  return check_tensor(dv, "dv", 16);
+}
+
+static cowa_status check_dq_ptrs(const void* q, const void* k, const void* v, const float* lse, const void* d_o,
+                                 const void* dq) {
+  COWA_TRY(check_qkv_lse_do(q, k, v, lse, d_o));
+  return check_tensor(dq, "dq", 16);
+}
+
 cowa_status cowa_bwd_prepare(const cowa_params* p, const void* o, const void* d_o, void* workspace, size_t ws_bytes,
                              void* stream) {
   float* dsum;
   COWA_TRY(check_bwd(p, ws_bytes, workspace, &dsum));
   if (p->batch == 0) return COWA_OK;
-  COWA_TRY(check_tensor(o, "o", 16));
-  COWA_TRY(check_tensor(d_o, "d_o", 16));
+  COWA_TRY(check_prepare_ptrs(o, d_o));
   COWA_TRY(check_device());
   return hip_status(cowa::launch_bwd_prepare(*p, o, d_o, dsum, static_cast<hipStream_t>(stream)),
                     "backward prepare launch");
@@ -307,11 +351,7 @@ cowa_status cowa_bwd_main(const cowa_params* p, const cowa_schedule_t* s, const 
   COWA_TRY(check_bwd(p, ws_bytes, workspace, &dsum));
   COWA_TRY(check_schedule(p, s));
   if (p->batch == 0) return COWA_OK;
-  COWA_TRY(check_qkv_lse_do(q, k, v, lse, d_o));
-  COWA_TRY(check_tensor(dk, "dk", 16));
-  COWA_TRY(check_tensor(dv, "dv", 16));
-  if ((int64_t)s->n_kt * p->h_k * p->batch >= (int64_t(1) << 31))
-    return fail(COWA_ERR_UNSUPPORTED, "too many key blocks for one launch");
+  COWA_TRY(check_main_ptrs(q, k, v, lse, d_o, dk, dv));
   COWA_TRY(check_device());
   return hip_status(cowa::launch_bwd_main(*p, cowa::sched_view(s), q, k, v, lse, d_o, dk, dv, dsum,
                                           static_cast<hipStream_t>(stream)),
@@ -325,16 +365,14 @@ cowa_status cowa_bwd_dq(const cowa_params* p, const cowa_schedule_t* s, const vo
   COWA_TRY(check_bwd(p, ws_bytes, workspace, &dsum));
   COWA_TRY(check_schedule(p, s));
   if (p->batch == 0) return COWA_OK;
-  COWA_TRY(check_qkv_lse_do(q, k, v, lse, d_o));
-  COWA_TRY(check_tensor(dq, "dq", 16));
-  if ((int64_t)s->n_qt * p->h_q * p->batch >= (int64_t(1) << 31))
-    return fail(COWA_ERR_UNSUPPORTED, "too many query blocks for one launch");
+  COWA_TRY(check_dq_ptrs(q, k, v, lse, d_o, dq));
   COWA_TRY(check_device());
   return hip_status(cowa::launch_bwd_dq(*p, cowa::sched_view(s), q, k, v, lse, d_o, dq, dsum,
                                         static_cast<hipStream_t>(stream)),
                     "backward dQ launch");
 }
 
+// All three stages; every check of every stage runs before the first launch.
 cowa_status cowa_bwd(const cowa_params* p, const cowa_schedule_t* s, const void* q, const void* k, const void* v,
                      const void* o, const float* lse, const void* d_o, void* dq, void* dk, void* dv, void* workspace,
                      size_t ws_bytes, void* stream) {
@@ -342,13 +380,15 @@ cowa_status cowa_bwd(const cowa_params* p, const cowa_schedule_t* s, const void*
   COWA_TRY(check_bwd(p, ws_bytes, workspace, &dsum));
   COWA_TRY(check_schedule(p, s));
   if (p->batch == 0) return COWA_OK;
-  const void* ptrs[] = {q, k, v, o, d_o, dq, dk, dv};
-  const char* names[] = {"q", "k", "v", "o", "d_o", "dq", "dk", "dv"};
-  for (int x = 0; x < 8; ++x) COWA_TRY(check_tensor(ptrs[x], names[x], 16));
-  COWA_TRY(check_tensor(lse, "lse", 4));
-  COWA_TRY(cowa_bwd_prepare(p, o, d_o, workspace, ws_bytes, stream));
-  COWA_TRY(cowa_bwd_main(p, s, q, k, v, lse, d_o, dk, dv, workspace, ws_bytes, stream));
-  return cowa_bwd_dq(p, s, q, k, v, lse, d_o, dq, workspace, ws_bytes, stream);
+  COWA_TRY(check_prepare_ptrs(o, d_o));
+  COWA_TRY(check_main_ptrs(q, k, v, lse, d_o, dk, dv));
+  COWA_TRY(check_dq_ptrs(q, k, v, lse, d_o, dq));
+  COWA_TRY(check_device());
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const cowa::SchedView sv = cowa::sched_view(s);
+  COWA_TRY(hip_status(cowa::launch_bwd_prepare(*p, o, d_o, dsum, st), "backward prepare launch"));
+  COWA_TRY(hip_status(cowa::launch_bwd_main(*p, sv, q, k, v, lse, d_o, dk, dv, dsum, st), "backward dK/dV launch"));
+  return hip_status(cowa::launch_bwd_dq(*p, sv, q, k, v, lse, d_o, dq, dsum, st), "backward dQ launch");
 }
 
 static cowa_status check_decode_params(const cowa_decode_params* p) {

@@ -450,12 +450,9 @@ hipError_t launch_main(const cowa_params& p, const SchedView& sv, const void* q,
   static_assert(C::OUT_BYTES <= C::LDS_MAX && C::MAIN_BYTES < C::LDS_MAX, "LDS budget");
   if (sv.n_qt > C::max_qblocks()) return hipErrorInvalidValue;
   auto kern = bwd_main<D, BK, NW>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_MAX);
+  {
+    const hipError_t err = allow_lds(reinterpret_cast<const void*>(kern), C::LDS_MAX);
     if (err != hipSuccess) return err;
-    attr_set = true;
   }
   const unsigned blocks = (unsigned)sv.n_kt * p.h_k * p.batch;
   hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * NW), C::lds_bytes(sv.n_qt), stream, p, sv,
@@ -737,12 +734,9 @@ hipError_t launch_dq_w(const cowa_params& p, const SchedView& sv, int hpw, int w
                        hipStream_t stream) {
   using C = DqCfg<D, BQ, BK, NQW>;
   auto kern = bwd_dq_kernel<D, BQ, BK, NQW, W4>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_MAX);
+  {
+    const hipError_t err = allow_lds(reinterpret_cast<const void*>(kern), C::LDS_MAX);
     if (err != hipSuccess) return err;
-    attr_set = true;
   }
   const int n_hgroups = p.h_q / hpw;
   const unsigned blocks = (unsigned)sv.n_qt * n_hgroups * p.batch;

@@ -541,12 +541,9 @@ hipError_t launch_waves(const cowa_params& p, const SchedView& sv, int hpw, int 
                         const void* k, const void* v, void* o, float* lse, hipStream_t stream) {
   using C = FwdCfg<D, BQ, BK>;
   auto kern = fwd_bf16_kernel<D, BQ, BK, FULL>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_MAX);
+  {
+    const hipError_t err = allow_lds(reinterpret_cast<const void*>(kern), C::LDS_MAX);
     if (err != hipSuccess) return err;
-    attr_set = true;
   }
   const unsigned blocks = (unsigned)sv.n_qt * n_hgroups * p.batch;
   hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * waves), C::lds_bytes(sv.n_kt), stream, p, sv, hpw,

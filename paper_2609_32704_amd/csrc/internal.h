@@ -29,6 +29,10 @@ inline SchedView sched_view(const cowa_schedule_t* s) {
   return v;
 }
 
+// Raise a kernel's dynamic LDS limit to `bytes`, once per (kernel, device);
+// thread-safe.  Called by the launchers before their first launch on a device.
+hipError_t allow_lds(const void* kernel, int bytes);
+
 // Each launcher enqueues on `stream` and returns hipGetLastError() of its launches.
 hipError_t launch_schedule(const cowa_schedule_t* s, hipStream_t stream);
 

@@ -233,3 +233,22 @@ def test_bwd_shape_limits_on_host(n_q, n_k, ok):
     else:
         assert st == abi.COWA_ERR_UNSUPPORTED
         assert b"blocks" in lib.cowa_last_error()
+
+
+def test_bwd_checks_every_stage_before_any_launch():
+    """cowa_bwd runs three stages; a limit of its last stage (the dQ pass's
+    grid of n_qt x h_q x batch workgroups) is rejected before the first stage
+    is launched: the status is COWA_ERR_UNSUPPORTED even without a device
+    (a launch attempt would need one and report COWA_ERR_NO_DEVICE)."""
+    lib = _lib()
+    bsz = (1 << 31) // (1000 * 64) + 1
+    p = cowa.make_params(bsz, 128000, 128000, 64, 1, 128, 128, 4096, 128, 128)
+    need = abi.cowa_bwd_workspace_size(p)
+    s = _sized(p)
+    vp = ctypes.c_void_p
+    st = lib.cowa_bwd(ctypes.byref(p), ctypes.byref(s), *[vp(1 << 24)] * 10, ctypes.c_size_t(need), vp(0))
+    assert st == abi.COWA_ERR_UNSUPPORTED
+    assert b"query blocks" in lib.cowa_last_error()
+    # each stage on its own applies the same check
+    st = lib.cowa_bwd_main(ctypes.byref(p), ctypes.byref(s), *[vp(1 << 24)] * 8, ctypes.c_size_t(need), vp(0))
+    assert st == abi.COWA_ERR_UNSUPPORTED
