@@ -52,18 +52,46 @@ typedef enum {
 
 typedef enum { COWA_BF16 = 0, COWA_FP32 = 1 } cowa_dtype;
 
-/* Per-KV-head window four-tuple of Sec. 2.1: (sink width, near width, gap
- * after the near window, long-range width) = (w_sink, w_near, b_h, b_{h+1} - b_h),
- * with L = max(N_k - w_sink - w_near, 0) and b_h = floor(h L / H_k)
- * (Eq. fwa_long_range_span). */
+/* Per-KV-head window four-tuple of Sec. 2.1 (the interface of Alg. 1 and
+ * Alg. 2): sink width, near width, gap after the near window, long-range
+ * width.  KV head h sees key i_k from query i_q iff, with the causal distance
+ * delta = i_q + (N_k - N_q) - i_k >= 0,
+ *     delta < near,  or  i_k < sink,  or  near + gap <= delta < near + gap + width.
+ * The default pattern (Eq. fwa_long_range_span) is (w_sink, w_near, b_h,
+ * b_{h+1} - b_h) with L = max(N_k - w_sink - w_near, 0), b_h = floor(h L / H_k)
+ * over the global KV-head index; Sec. 2.1 notes that the same interface
+ * permits head-specific widths and gaps, e.g. the m-window layouts of the
+ * collective-coverage ablation (App. A.1, Table 1).  All fields >= 0. */
 typedef struct {
   int32_t sink, near, gap, width;
 } cowa_window;
 
-/* Shapes and windows of one forward/backward call. */
+/* Shapes and windows of one forward/backward call.
+ *
+ * Fixed lengths (cu_seqlens_q == NULL): B sequences of N_q queries and N_k
+ * keys; tensors [B, H, N, d] as described above.
+ *
+ * Ragged batch (cu_seqlens_q and cu_seqlens_k non-NULL; Eq. fwa_distance
+ * aligns each sequence's queries to the end of its own keys, which is what
+ * variable-length prefill needs): sequence b has queries
+ * [cu_seqlens_q[b], cu_seqlens_q[b+1]) and keys [cu_seqlens_k[b],
+ * cu_seqlens_k[b+1]) of the packed tensors Q, O, dO, dQ [H_q, N_q, d] and K,
+ * V, dK, dV [H_k, N_k, d] (LSE [H_q, N_q]), where n_q = cu_seqlens_q[B] and
+ * n_k = cu_seqlens_k[B] are the packed totals.  Both arrays are host int32
+ * [batch + 1], start at 0, never decrease, and 0 <= N_q(b) <= N_k(b) for every
+ * sequence; a query of sequence b never sees a key of another sequence.
+ *
+ * Windows: windows == NULL takes the default rule from w_sink, w_near,
+ * h_k_total and h_k_offset (per sequence from its own N_k when ragged);
+ * otherwise windows points to h_k host tuples, one per local KV head, used
+ * as given for every sequence (w_sink, w_near, h_k_total, h_k_offset are then
+ * not used for the windows).
+ *
+ * The host arrays are read by the call that receives them and not kept, except
+ * that a schedule records a digest of their values (see cowa_schedule_t). */
 typedef struct {
   int32_t batch;          /* B >= 0; B = 0 is a no-op */
-  int32_t n_q, n_k;       /* 1 <= N_q <= N_k < 2^30 */
+  int32_t n_q, n_k;       /* fixed: 1 <= N_q <= N_k < 2^30; ragged: the packed totals (< 2^30) */
   int32_t h_q, h_k;       /* local heads on this device; H_q % H_k == 0 */
   int32_t head_dim;       /* 64 or 128 */
   int32_t w_sink, w_near; /* >= 0 */
@@ -72,6 +100,9 @@ typedef struct {
   int32_t tile_q, tile_k; /* block sizes B_q, B_k: 32, 64 or 128 */
   float softmax_scale;    /* > 0, multiplies Q K^T (1/sqrt(d) for the standard scale) */
   int32_t dtype;          /* cowa_dtype */
+  const cowa_window* windows;    /* NULL (default rule) or h_k host tuples */
+  const int32_t* cu_seqlens_q;   /* NULL (fixed lengths) or host int32 [batch + 1] */
+  const int32_t* cu_seqlens_k;   /* NULL iff cu_seqlens_q is NULL */
 } cowa_params;
 
 /* Block schedule (Sec. 2.3): for every local KV head h and QO block i the KV
@@ -83,15 +114,26 @@ typedef struct {
  *   bwd_col_ptr  int32 [h_k * n_kt + 1]   column c = h * n_kt + j
  *   fwd_ent      uint32[nnz]  (j << 1) | partial, j descending in a row (Alg. 1)
  *   bwd_ent      uint32[nnz]  (i << 1) | partial, i ascending in a column (Alg. 2)
- * partial = 0 (FULL) iff all B_q * B_k element pairs of the tile lie inside
- * both sequences and are legal; only partial tiles are masked element-wise. */
+ *   then internal tables (resolved windows; sequence table and block-to-
+ *   sequence maps of a ragged batch) at off_windows .. bytes.
+ * In a ragged batch i and j count the blocks over the whole batch (the blocks
+ * of sequence b follow those of sequence b - 1; each sequence starts a new
+ * block), while the entries hold blocks within the sequence.  partial = 0
+ * (FULL) iff all B_q * B_k element pairs of the tile lie inside the sequence
+ * and are legal; only partial tiles are masked element-wise.
+ * `p` is a copy of the sizing parameters: its pointer fields must still hold
+ * the same values when cowa_schedule is called (checked against `digest`),
+ * and cowa_fwd / cowa_bwd compare the digest of their own parameters. */
 typedef struct {
   cowa_params p;          /* the parameters it was sized for */
-  int32_t n_qt, n_kt;     /* ceil(N_q / B_q), ceil(N_k / B_k) */
+  int32_t n_qt, n_kt;     /* QO / KV blocks: ceil(N / B) per sequence, or summed over a ragged batch */
   int32_t max_row;        /* longest J_h(i) */
   int32_t max_col;        /* longest I_h(j) */
-  int64_t nnz;            /* listed tiles over the local KV heads */
+  int64_t nnz;            /* listed tiles over the local KV heads (and sequences, when ragged) */
   size_t off_fwd_row_ptr, off_bwd_col_ptr, off_fwd_ent, off_bwd_ent; /* byte offsets in buf */
+  size_t off_windows, off_seqs, off_qt_seq, off_kt_seq;            /* internal tables */
+  int32_t max_qt, max_kt; /* QO / KV blocks of the longest sequence */
+  uint64_t digest;        /* of the window tuples and sequence lengths it was sized for */
   size_t bytes;           /* size of buf */
   void* buf;              /* device buffer, set by the caller */
 } cowa_schedule_t;
@@ -108,6 +150,8 @@ typedef struct {
                              default: ~1024 programs in total, each >= 256 keys */
   float softmax_scale;    /* > 0 */
   int32_t dtype;          /* COWA_BF16 */
+  const cowa_window* windows;  /* NULL: default rule from each sequence's N_k; else h_k host
+                                  tuples (at most 256 local KV heads), the same for every sequence */
 } cowa_decode_params;
 
 /* Library version string. */
@@ -118,11 +162,15 @@ const char* cowa_last_error(void);
 
 /* Window tuples of the h_k local KV heads for key length n_k (Sec. 2.1,
  * Eq. fwa_long_range_span, Eq. fwa_global_head).  Host only; out_host has
- * p->h_k entries.  Computed in 64-bit integers. */
+ * p->h_k entries.  Computed in 64-bit integers.  With explicit windows they
+ * are returned as given; for a ragged batch under the default rule each
+ * sequence has its own tuples (from its N_k): this returns those of key
+ * length p->n_k. */
 cowa_status cowa_windows(const cowa_params* p, cowa_window* out_host);
 
 /* Size the schedule of `p` (Sec. 2.3; tile sets are the paper's J_h(i) and
- * I_h(j)): fills every field of *out except buf.  Host only, O(h_k (n_qt + n_kt)). */
+ * I_h(j)): fills every field of *out except buf.  Host only, O(h_k (n_qt + n_kt)).
+ * Validates the windows and sequence lengths (COWA_ERR_INVALID_ARG). */
 cowa_status cowa_schedule_size(const cowa_params* p, cowa_schedule_t* out);
 
 /* Work accounting (host only): the number of legal (query, key) pairs of
@@ -135,8 +183,10 @@ cowa_status cowa_legal_pairs(const cowa_params* p, int64_t* pairs);
  * each is one K row and one V row read.  Invalid lengths count zero. */
 cowa_status cowa_decode_visible_keys(const cowa_decode_params* p, const int32_t* seqlens_host, int64_t* keys);
 
-/* Build the schedule into s->buf on the device (three small kernels:
- * per-row counts, prefix sums, entry fill). */
+/* Build the schedule into s->buf on the device: the window (and sequence)
+ * tables, then three small kernels: per-row counts, prefix sums, entry fill.
+ * The host arrays of s->p are read during the call (they are copied into the
+ * kernels' arguments), so they may be freed as soon as it returns. */
 cowa_status cowa_schedule(const cowa_schedule_t* s, void* stream);
 
 /* Forward (Alg. 1): O and LSE of masked softmax attention over each query's

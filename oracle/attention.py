@@ -38,13 +38,20 @@ gather, so the result is the same exact definition.
 
 import numpy as np
 
-from .windows import kv_head_of, visible_mask, visible_intervals
+from .windows import kv_head_of, visible_mask_bounds, visible_intervals_bounds, head_bounds
 
 
-def _union_keys(rows, n_q, n_k, w_sink, w_near, h_global, h_total):
+def _bounds(n_k, w_sink, w_near, h_offset, hk, h_total, windows):
+    """(sink, near, lo, hi) of local KV head hk: its explicit four-tuple when
+    ``windows`` (one (sink, near, gap, width) per local KV head) is given, else
+    the default rule over the global head index (Sec. 2.1)."""
+    return head_bounds(n_k, w_sink, w_near, h_offset + hk, h_total, None if windows is None else windows[hk])
+
+
+def _union_keys(rows, n_q, n_k, bounds):
     runs = []
     for i_q in rows:
-        runs += visible_intervals(int(i_q), n_q, n_k, w_sink, w_near, h_global, h_total)
+        runs += visible_intervals_bounds(int(i_q), n_q, n_k, *bounds)
     if not runs:
         return np.zeros(0, dtype=np.int64)
     runs.sort()
@@ -57,19 +64,20 @@ def _union_keys(rows, n_q, n_k, w_sink, w_near, h_global, h_total):
     return np.concatenate([np.arange(a, b, dtype=np.int64) for a, b in merged])
 
 
-def _rows_forward(qh, kh, vh, rows, n_q, n_k, w_sink, w_near, h_global, h_total, scale):
-    """Exact O and LSE of the given query rows of one (batch, QO head).
+def _rows_forward(qh, kh, vh, rows, n_q, n_k, bounds, scale):
+    """Exact O and LSE of the given query rows of one (batch, QO head) whose
+    KV head has the window bounds (sink, near, lo, hi).
 
     qh [N_q, d]; kh, vh [N_k, d]; rows: sorted int array (a block of nearby rows).
     Returns (o [len(rows), d], lse [len(rows)], keys, p) where ``keys`` are the
     gathered key positions and p the normalised probabilities on them.
     """
-    keys = _union_keys(rows, n_q, n_k, w_sink, w_near, h_global, h_total)
+    keys = _union_keys(rows, n_q, n_k, bounds)
     d = qh.shape[1]
     if keys.size == 0:
         return (np.zeros((len(rows), d)), np.full(len(rows), -np.inf), keys,
                 np.zeros((len(rows), 0)))
-    mask = visible_mask(n_q, n_k, w_sink, w_near, h_global, h_total, rows=rows, cols=keys)
+    mask = visible_mask_bounds(n_q, n_k, *bounds, rows=rows, cols=keys)
     s = scale * (qh[rows] @ kh[keys].T)
     s = np.where(mask, s, -np.inf)
     m = s.max(axis=1)
@@ -88,8 +96,9 @@ def _blocks(rows, size):
         yield rows[s:s + size]
 
 
-def forward(q, k, v, w_sink, w_near, scale, h_total=None, h_offset=0, block=256):
-    """Full forward: returns (O, LSE) in float64."""
+def forward(q, k, v, w_sink, w_near, scale, h_total=None, h_offset=0, block=256, windows=None):
+    """Full forward: returns (O, LSE) in float64.  ``windows``: None (default
+    rule) or one (sink, near, gap, width) tuple per local KV head."""
     q, k, v = (np.asarray(x, dtype=np.float64) for x in (q, k, v))
     bsz, h_q, n_q, d = q.shape
     h_k, n_k = k.shape[1], k.shape[2]
@@ -99,15 +108,15 @@ def forward(q, k, v, w_sink, w_near, scale, h_total=None, h_offset=0, block=256)
     for b in range(bsz):
         for h in range(h_q):
             hk = kv_head_of(h, h_q, h_k)
+            bounds = _bounds(n_k, w_sink, w_near, h_offset, hk, h_total, windows)
             for rows in _blocks(np.arange(n_q), block):
-                ob, lb, _, _ = _rows_forward(q[b, h], k[b, hk], v[b, hk], rows, n_q, n_k,
-                                             w_sink, w_near, h_offset + hk, h_total, scale)
+                ob, lb, _, _ = _rows_forward(q[b, h], k[b, hk], v[b, hk], rows, n_q, n_k, bounds, scale)
                 o[b, h, rows] = ob
                 lse[b, h, rows] = lb
     return o, lse
 
 
-def forward_rows(q, k, v, rows, w_sink, w_near, scale, h_total=None, h_offset=0, block=128):
+def forward_rows(q, k, v, rows, w_sink, w_near, scale, h_total=None, h_offset=0, block=128, windows=None):
     """O and LSE of selected rows.  ``rows``: iterable of (b, h, i_q).
     Returns (o [n, d], lse [n]) in the order given."""
     q, k, v = (np.asarray(x, dtype=np.float64) for x in (q, k, v))
@@ -123,18 +132,19 @@ def forward_rows(q, k, v, rows, w_sink, w_near, scale, h_total=None, h_offset=0,
     for (b, h), lst in groups.items():
         lst.sort()
         hk = kv_head_of(h, h_q, h_k)
+        bounds = _bounds(n_k, w_sink, w_near, h_offset, hk, h_total, windows)
         for s in range(0, len(lst), block):
             chunk = lst[s:s + block]
             idx = np.array([i for i, _ in chunk], dtype=np.int64)
-            ob, lb, _, _ = _rows_forward(q[b, h], k[b, hk], v[b, hk], idx, n_q, n_k,
-                                         w_sink, w_near, h_offset + hk, h_total, scale)
+            ob, lb, _, _ = _rows_forward(q[b, h], k[b, hk], v[b, hk], idx, n_q, n_k, bounds, scale)
             for t, (_, n) in enumerate(chunk):
                 out_o[n] = ob[t]
                 out_l[n] = lb[t]
     return out_o, out_l
 
 
-def backward(q, k, v, do, w_sink, w_near, scale, h_total=None, h_offset=0, block=256, rows=None, heads=None):
+def backward(q, k, v, do, w_sink, w_near, scale, h_total=None, h_offset=0, block=256, rows=None, heads=None,
+             windows=None):
     """Exact gradient of <dO, O(Q, K, V)>.  Returns (dQ, dK, dV, O, LSE).
 
     ``rows`` / ``heads`` restrict the work to those query rows and QO heads
@@ -152,9 +162,9 @@ def backward(q, k, v, do, w_sink, w_near, scale, h_total=None, h_offset=0, block
     for b in range(bsz):
         for h in (range(h_q) if heads is None else heads):
             hk = kv_head_of(h, h_q, h_k)
+            bounds = _bounds(n_k, w_sink, w_near, h_offset, hk, h_total, windows)
             for rows in _blocks(row_set, block):
-                ob, lb, keys, p = _rows_forward(q[b, h], k[b, hk], v[b, hk], rows, n_q, n_k,
-                                                w_sink, w_near, h_offset + hk, h_total, scale)
+                ob, lb, keys, p = _rows_forward(q[b, h], k[b, hk], v[b, hk], rows, n_q, n_k, bounds, scale)
                 o[b, h, rows] = ob
                 lse[b, h, rows] = lb
                 if keys.size == 0:
@@ -169,7 +179,7 @@ def backward(q, k, v, do, w_sink, w_near, scale, h_total=None, h_offset=0, block
 
 
 def backward_kv_rows(q, k, v, do, kv_rows, w_sink, w_near, scale, h_total=None, h_offset=0,
-                     block=128):
+                     block=128, windows=None):
     """Exact dK and dV of selected key rows.  ``kv_rows``: iterable of
     (b, h_k, i_k).  Every query that sees one of the selected keys is
     evaluated over its whole visible set (its O and LSE are needed).
@@ -189,17 +199,16 @@ def backward_kv_rows(q, k, v, do, kv_rows, w_sink, w_near, scale, h_total=None, 
         pos = {int(i): t for t, i in enumerate(sel)}
         acc_k = np.zeros((len(sel), k.shape[3]))
         acc_v = np.zeros((len(sel), v.shape[3]))
+        bounds = _bounds(n_k, w_sink, w_near, h_offset, hk, h_total, windows)
         # queries that see at least one selected key, per QO head of the group
         for h in range(h_q):
             if kv_head_of(h, h_q, h_k) != hk:
                 continue
             sees = np.zeros(n_q, dtype=bool)
             for rows in _blocks(np.arange(n_q), 4096):
-                sees[rows] = visible_mask(n_q, n_k, w_sink, w_near, h_offset + hk, h_total,
-                                          rows=rows, cols=sel).any(axis=1)
+                sees[rows] = visible_mask_bounds(n_q, n_k, *bounds, rows=rows, cols=sel).any(axis=1)
             for rows in _blocks(np.nonzero(sees)[0], block):
-                ob, lb, keys, p = _rows_forward(q[b, h], k[b, hk], v[b, hk], rows, n_q, n_k,
-                                                w_sink, w_near, h_offset + hk, h_total, scale)
+                ob, lb, keys, p = _rows_forward(q[b, h], k[b, hk], v[b, hk], rows, n_q, n_k, bounds, scale)
                 dp = do[b, h, rows] @ v[b, hk, keys].T
                 dsum = (ob * do[b, h, rows]).sum(axis=1)
                 ds = p * (dp - dsum[:, None])
@@ -214,7 +223,7 @@ def backward_kv_rows(q, k, v, do, kv_rows, w_sink, w_near, scale, h_total=None, 
     return out_dk, out_dv
 
 
-def backward_q_rows(q, k, v, do, rows, w_sink, w_near, scale, h_total=None, h_offset=0, block=128):
+def backward_q_rows(q, k, v, do, rows, w_sink, w_near, scale, h_total=None, h_offset=0, block=128, windows=None):
     """Exact dQ (and O, LSE) of selected query rows ``(b, h, i_q)``, evaluated in
     blocks of nearby rows of one (batch, QO head).
     Returns (dq [n, d], o [n, d], lse [n]) in the order given."""
@@ -232,11 +241,11 @@ def backward_q_rows(q, k, v, do, rows, w_sink, w_near, scale, h_total=None, h_of
     for (b, h), lst in groups.items():
         lst.sort()
         hk = kv_head_of(h, h_q, h_k)
+        bounds = _bounds(n_k, w_sink, w_near, h_offset, hk, h_total, windows)
         for s in range(0, len(lst), block):
             chunk = lst[s:s + block]
             idx = np.array([i for i, _ in chunk], dtype=np.int64)
-            ob, lb, keys, p = _rows_forward(q[b, h], k[b, hk], v[b, hk], idx, n_q, n_k,
-                                            w_sink, w_near, h_offset + hk, h_total, scale)
+            ob, lb, keys, p = _rows_forward(q[b, h], k[b, hk], v[b, hk], idx, n_q, n_k, bounds, scale)
             dqb = np.zeros((len(idx), q.shape[3]))
             if keys.size:
                 dp = do[b, h, idx] @ v[b, hk, keys].T
@@ -248,7 +257,7 @@ def backward_q_rows(q, k, v, do, rows, w_sink, w_near, scale, h_total=None, h_of
     return out_dq, out_o, out_l
 
 
-def decode(q, k_cache, v_cache, seqlens, w_sink, w_near, scale, h_total=None, h_offset=0):
+def decode(q, k_cache, v_cache, seqlens, w_sink, w_near, scale, h_total=None, h_offset=0, windows=None):
     """One decoding step (Sec. 2.3, decoding execution): the forward with N_q = 1
     per sequence, N_k = seqlens[b] (cached tokens plus the current one, whose
     K/V the caller has already appended), breakpoints from that N_k.
@@ -264,8 +273,49 @@ def decode(q, k_cache, v_cache, seqlens, w_sink, w_near, scale, h_total=None, h_
         n_k = int(seqlens[b])
         for h in range(h_q):
             hk = kv_head_of(h, h_q, h_k)
+            bounds = _bounds(n_k, w_sink, w_near, h_offset, hk, h_total, windows)
             ob, lb, _, _ = _rows_forward(q[b, h][None, :], kc[b, hk, :n_k], vc[b, hk, :n_k],
-                                         np.array([0]), 1, n_k, w_sink, w_near, h_offset + hk,
-                                         h_total, scale)
+                                         np.array([0]), 1, n_k, bounds, scale)
             o[b, h], lse[b, h] = ob[0], lb[0]
     return o, lse
+
+
+def _seq_slices(cu_q, cu_k):
+    cu_q = [int(x) for x in cu_q]
+    cu_k = [int(x) for x in cu_k]
+    return [(slice(cu_q[b], cu_q[b + 1]), slice(cu_k[b], cu_k[b + 1])) for b in range(len(cu_q) - 1)]
+
+
+def forward_varlen(q, k, v, cu_q, cu_k, w_sink, w_near, scale, h_total=None, h_offset=0, windows=None):
+    """Forward of a ragged batch: sequence b has queries cu_q[b] .. cu_q[b+1] of
+    the packed q [H_q, N_q, d] and keys cu_k[b] .. cu_k[b+1] of k, v [H_k, N_k, d];
+    each sequence is its own attention problem, its queries aligned to the end
+    of its own keys (Eq. fwa_distance), run through ``forward`` one at a time.
+    Returns (O [H_q, N_q, d], LSE [H_q, N_q])."""
+    q, k, v = (np.asarray(x, dtype=np.float64) for x in (q, k, v))
+    o = np.zeros((q.shape[0], q.shape[1], v.shape[2]))
+    lse = np.zeros((q.shape[0], q.shape[1]))
+    for sq, sk in _seq_slices(cu_q, cu_k):
+        if sq.stop == sq.start:
+            continue
+        ob, lb = forward(q[None, :, sq], k[None, :, sk], v[None, :, sk], w_sink, w_near, scale, h_total, h_offset,
+                         windows=windows)
+        o[:, sq], lse[:, sq] = ob[0], lb[0]
+    return o, lse
+
+
+def backward_varlen(q, k, v, do, cu_q, cu_k, w_sink, w_near, scale, h_total=None, h_offset=0, windows=None):
+    """Gradient of a ragged batch, one sequence at a time through ``backward``
+    (keys of a sequence without queries get zero gradients).
+    Returns (dQ, dK, dV, O, LSE) in the packed layouts."""
+    q, k, v, do = (np.asarray(x, dtype=np.float64) for x in (q, k, v, do))
+    dq, dk, dv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
+    o = np.zeros_like(do)
+    lse = np.zeros((q.shape[0], q.shape[1]))
+    for sq, sk in _seq_slices(cu_q, cu_k):
+        if sq.stop == sq.start:
+            continue
+        r = backward(q[None, :, sq], k[None, :, sk], v[None, :, sk], do[None, :, sq], w_sink, w_near, scale,
+                     h_total, h_offset, windows=windows)
+        dq[:, sq], dk[:, sk], dv[:, sk], o[:, sq], lse[:, sq] = (x[0] for x in r)
+    return dq, dk, dv, o, lse

@@ -23,7 +23,7 @@ rectangle lies inside the sequences (i_q < N_q, i_k < N_k) and is legal.
 
 import numpy as np
 
-from .windows import visible_mask, visible_intervals
+from .windows import visible_mask_bounds, visible_intervals_bounds, head_bounds
 
 
 def _pack(row_lists, n_rows):
@@ -55,7 +55,7 @@ def _assemble(listed, full, n_qt, n_kt):
             "n_qt": n_qt, "n_kt": n_kt, "listed": listed, "full": full}
 
 
-def tile_flags_bruteforce(n_q, n_k, tile_q, tile_k, w_sink, w_near, h_k, h_total, h_offset):
+def tile_flags_bruteforce(n_q, n_k, tile_q, tile_k, w_sink, w_near, h_k, h_total, h_offset, windows=None):
     """Method A: reduce the element mask over every tile rectangle.
 
     Out-of-sequence positions are padded as illegal, so a tile that sticks out
@@ -67,7 +67,8 @@ def tile_flags_bruteforce(n_q, n_k, tile_q, tile_k, w_sink, w_near, h_k, h_total
     listed = np.zeros((h_k, n_qt, n_kt), dtype=bool)
     full = np.zeros((h_k, n_qt, n_kt), dtype=bool)
     for h in range(h_k):
-        m = visible_mask(n_q, n_k, w_sink, w_near, h_offset + h, h_total)
+        bounds = head_bounds(n_k, w_sink, w_near, h_offset + h, h_total, None if windows is None else windows[h])
+        m = visible_mask_bounds(n_q, n_k, *bounds)
         pad = np.zeros((n_qt * tile_q, n_kt * tile_k), dtype=bool)
         pad[:n_q, :n_k] = m
         blocks = pad.reshape(n_qt, tile_q, n_kt, tile_k)
@@ -76,7 +77,7 @@ def tile_flags_bruteforce(n_q, n_k, tile_q, tile_k, w_sink, w_near, h_k, h_total
     return listed, full
 
 
-def tile_flags_intervals(n_q, n_k, tile_q, tile_k, w_sink, w_near, h_k, h_total, h_offset):
+def tile_flags_intervals(n_q, n_k, tile_q, tile_k, w_sink, w_near, h_k, h_total, h_offset, windows=None):
     """Method B: per query, the merged key runs of A_h(i_q) mark the tiles they
     touch and the tiles they cover completely.
 
@@ -95,9 +96,10 @@ def tile_flags_intervals(n_q, n_k, tile_q, tile_k, w_sink, w_near, h_k, h_total,
         cover = np.zeros((n_qt, n_kt + 1), dtype=np.int64)
         rows_t, cols_t, vals_t = [], [], []
         rows_c, cols_c, vals_c = [], [], []
+        bounds = head_bounds(n_k, w_sink, w_near, h_offset + h, h_total, None if windows is None else windows[h])
         for i_q in range(n_q):
             qt = i_q // tile_q
-            for a, b in visible_intervals(i_q, n_q, n_k, w_sink, w_near, h_offset + h, h_total):
+            for a, b in visible_intervals_bounds(i_q, n_q, n_k, *bounds):
                 ja, jb = a // tile_k, (b - 1) // tile_k          # touched blocks [ja, jb]
                 rows_t += [qt, qt]
                 cols_t += [ja, jb + 1]
@@ -114,16 +116,58 @@ def tile_flags_intervals(n_q, n_k, tile_q, tile_k, w_sink, w_near, h_k, h_total,
                       np.asarray(vals_c, dtype=np.int64))
         listed[h] = np.cumsum(touch, axis=1)[:, :n_kt] > 0
         covered_by = np.cumsum(cover, axis=1)[:, :n_kt]
-        q_inside = np.array([(i + 1) * tile_q <= n_q for i in range(n_qt)])
-        k_inside = np.array([(j + 1) * tile_k <= n_k for j in range(n_kt)])
+        q_inside = np.array([(i + 1) * tile_q <= n_q for i in range(n_qt)], dtype=bool)
+        k_inside = np.array([(j + 1) * tile_k <= n_k for j in range(n_kt)], dtype=bool)
         full[h] = (covered_by == tile_q) & q_inside[:, None] & k_inside[None, :]
     return listed, full
 
 
-def build(n_q, n_k, tile_q, tile_k, w_sink, w_near, h_k, h_total=None, h_offset=0, method="intervals"):
-    """Canonical CSR schedule of the local KV heads (see the module docstring)."""
+def build(n_q, n_k, tile_q, tile_k, w_sink, w_near, h_k, h_total=None, h_offset=0, method="intervals",
+          windows=None):
+    """Canonical CSR schedule of the local KV heads (see the module docstring).
+    ``windows``: None (default rule) or one (sink, near, gap, width) per head."""
     if h_total is None:
         h_total = h_k
     fn = tile_flags_intervals if method == "intervals" else tile_flags_bruteforce
-    listed, full = fn(n_q, n_k, tile_q, tile_k, w_sink, w_near, h_k, h_total, h_offset)
+    listed, full = fn(n_q, n_k, tile_q, tile_k, w_sink, w_near, h_k, h_total, h_offset, windows)
     return _assemble(listed, full, listed.shape[1], listed.shape[2])
+
+
+def build_varlen(cu_q, cu_k, tile_q, tile_k, w_sink, w_near, h_k, h_total=None, h_offset=0, method="intervals",
+                 windows=None):
+    """Canonical CSR schedule of a ragged batch: each sequence's blocks are
+    found from its own lengths (its queries aligned to the end of its keys,
+    Eq. fwa_distance), and the blocks of sequence b follow those of b - 1:
+    row h * n_qt + (first block of b) + i, column h * n_kt + (first block of b)
+    + j, with n_qt / n_kt the block counts over the batch; entries hold blocks
+    within the sequence."""
+    if h_total is None:
+        h_total = h_k
+    fn = tile_flags_intervals if method == "intervals" else tile_flags_bruteforce
+    per = []
+    for b in range(len(cu_q) - 1):
+        n_q, n_k = int(cu_q[b + 1] - cu_q[b]), int(cu_k[b + 1] - cu_k[b])
+        if n_k == 0:
+            per.append(None)
+            continue
+        per.append(fn(n_q, n_k, tile_q, tile_k, w_sink, w_near, h_k, h_total, h_offset, windows))
+    fwd_rows, bwd_cols = [], []
+    for h in range(h_k):
+        for flags in per:
+            if flags is None:
+                continue
+            listed, full = flags
+            for i in range(listed.shape[1]):
+                js = np.nonzero(listed[h, i])[0][::-1]
+                fwd_rows.append([(int(j) << 1) | int(not full[h, i, j]) for j in js])
+        for flags in per:
+            if flags is None:
+                continue
+            listed, full = flags
+            for j in range(listed.shape[2]):
+                is_ = np.nonzero(listed[h, :, j])[0]
+                bwd_cols.append([(int(i) << 1) | int(not full[h, i, j]) for i in is_])
+    fwd_row_ptr, fwd_ent = _pack(fwd_rows, len(fwd_rows))
+    bwd_col_ptr, bwd_ent = _pack(bwd_cols, len(bwd_cols))
+    return {"fwd_row_ptr": fwd_row_ptr, "fwd_ent": fwd_ent, "bwd_col_ptr": bwd_col_ptr, "bwd_ent": bwd_ent,
+            "n_qt": len(fwd_rows) // h_k, "n_kt": len(bwd_cols) // h_k}

@@ -54,8 +54,26 @@ def long_window_bounds(n_k, w_sink, w_near, h_global, h_total):
     return w_near + b[h_global], w_near + b[h_global + 1]
 
 
-def visible_mask(n_q, n_k, w_sink, w_near, h_global, h_total, rows=None, cols=None):
-    """Element mask M[i_q, i_k] of the visible-key set A_h(i_q) (Eq. fwa_support).
+def tuple_bounds(window):
+    """Distance bounds of a four-tuple (sink, near, gap, width) (Sec. 2.1:
+    sink width, near width, gap after the near window, long-range width):
+    (sink, near, lo, hi) with the long window near + gap <= delta < near + gap + width."""
+    sink, near, gap, width = (int(x) for x in window)
+    return sink, near, near + gap, near + gap + width
+
+
+def head_bounds(n_k, w_sink, w_near, h_global, h_total, window=None):
+    """(sink, near, lo, hi) of one KV head: from its explicit four-tuple if one
+    is given, else from the default rule (Eq. fwa_long_range_span)."""
+    if window is not None:
+        return tuple_bounds(window)
+    lo, hi = long_window_bounds(n_k, w_sink, w_near, h_global, h_total)
+    return w_sink, w_near, lo, hi
+
+
+def visible_mask_bounds(n_q, n_k, sink, near, lo, hi, rows=None, cols=None):
+    """Element mask M[i_q, i_k] of A(i_q) = near u sink u long (Eq. fwa_support)
+    for the window bounds (sink, near, lo, hi).
 
     The three windows of Sec. 2.1 are built separately and joined with a
     logical OR, i.e. a set union: a key that lies in two windows is still one
@@ -65,44 +83,68 @@ def visible_mask(n_q, n_k, w_sink, w_near, h_global, h_total, rows=None, cols=No
     iq = np.arange(n_q, dtype=np.int64) if rows is None else np.asarray(rows, dtype=np.int64)
     ik = np.arange(n_k, dtype=np.int64) if cols is None else np.asarray(cols, dtype=np.int64)
     delta = causal_distance(iq[:, None], ik[None, :], n_q, n_k)
-    lo, hi = long_window_bounds(n_k, w_sink, w_near, h_global, h_total)
-    near = (delta >= 0) & (delta < w_near)
-    sink = (ik[None, :] < w_sink) & (delta >= 0)
+    near_w = (delta >= 0) & (delta < near)
+    sink_w = (ik[None, :] < sink) & (delta >= 0)
     far = (delta >= lo) & (delta < hi)
-    return near | sink | far
+    return near_w | sink_w | far
 
 
-def visible_set(i_q, n_q, n_k, w_sink, w_near, h_global, h_total):
+def visible_mask(n_q, n_k, w_sink, w_near, h_global, h_total, rows=None, cols=None):
+    """The mask of the default pattern's KV head h_global (Eq. fwa_support)."""
+    lo, hi = long_window_bounds(n_k, w_sink, w_near, h_global, h_total)
+    return visible_mask_bounds(n_q, n_k, w_sink, w_near, lo, hi, rows, cols)
+
+
+def m_window_layout(n_k, w_sink, w_near, h_k, m):
+    """The m-window layouts of the collective-coverage ablation (App. A.1,
+    Table 1): the long-range history is cut into H_k equal-width regions W_1 ..
+    W_{H_k}, W_1 next to the near window (the default pattern's long window of
+    KV head 0) and W_{H_k} next to the sink; the m regions closest to the near
+    window, W_1 .. W_m, are repeated across the H_k KV heads (head h takes
+    W_{(h mod m) + 1}), with the shared sink and near windows unchanged.
+    Returns one (sink, near, gap, width) tuple per KV head; m = H_k is the
+    default pattern."""
+    if h_k % m != 0:
+        raise ValueError("m must divide the number of KV heads")
+    return [window_tuple(n_k, w_sink, w_near, h % m, h_k) for h in range(h_k)]
+
+
+def visible_set(i_q, n_q, n_k, w_sink, w_near, h_global, h_total, window=None):
     """The same set A_h(i_q), built element by element with Python sets (for
-    tiny brute-force checks; independent of the vectorised mask above)."""
-    span = max(n_k - w_sink - w_near, 0)
-    b_lo = (h_global * span) // h_total
-    b_hi = ((h_global + 1) * span) // h_total
+    tiny brute-force checks; independent of the vectorised mask above).  With
+    ``window`` = (sink, near, gap, width) the head's explicit four-tuple is used
+    as Sec. 2.1 defines it instead of the default rule."""
+    if window is None:
+        span = max(n_k - w_sink - w_near, 0)
+        b_lo = (h_global * span) // h_total
+        b_hi = ((h_global + 1) * span) // h_total
+        sink_w, near_w, gap, width = w_sink, w_near, b_lo, b_hi - b_lo
+    else:
+        sink_w, near_w, gap, width = window
     near, sink, far = set(), set(), set()
     for i_k in range(n_k):
         d = i_q + (n_k - n_q) - i_k
-        if 0 <= d < w_near:
+        if 0 <= d < near_w:
             near.add(i_k)
-        if i_k < w_sink and d >= 0:
+        if i_k < sink_w and d >= 0:
             sink.add(i_k)
-        if w_near + b_lo <= d < w_near + b_hi:
+        if near_w + gap <= d < near_w + gap + width:
             far.add(i_k)
     return near | sink | far
 
 
-def visible_intervals(i_q, n_q, n_k, w_sink, w_near, h_global, h_total):
-    """A_h(i_q) as a sorted list of disjoint, non-touching half-open key
-    intervals [a, b).
+def visible_intervals_bounds(i_q, n_q, n_k, sink, near, lo, hi):
+    """A(i_q) for the window bounds (sink, near, lo, hi) as a sorted list of
+    disjoint, non-touching half-open key intervals [a, b).
 
     Each window of Sec. 2.1 is a contiguous run of keys: with c = i_q + N_k - N_q
     the key at distance 0, delta in [x, y) is the key run (c - y, c - x].  The
     runs are clipped to [0, N_k) and merged (union, touching runs joined).
     """
     c = i_q + (n_k - n_q)
-    lo, hi = long_window_bounds(n_k, w_sink, w_near, h_global, h_total)
     runs = [
-        (c - w_near + 1, c + 1),          # near: 0 <= delta < w_near
-        (0, min(w_sink, c + 1)),          # sink: i_k < w_sink and delta >= 0
+        (c - near + 1, c + 1),            # near: 0 <= delta < near
+        (0, min(sink, c + 1)),            # sink: i_k < sink and delta >= 0
         (c - hi + 1, c - lo + 1),         # long: lo <= delta < hi
     ]
     clipped = []
@@ -120,29 +162,43 @@ def visible_intervals(i_q, n_q, n_k, w_sink, w_near, h_global, h_total):
     return merged
 
 
+def visible_intervals(i_q, n_q, n_k, w_sink, w_near, h_global, h_total):
+    """A_h(i_q) of the default pattern's KV head h_global as disjoint key intervals."""
+    lo, hi = long_window_bounds(n_k, w_sink, w_near, h_global, h_total)
+    return visible_intervals_bounds(i_q, n_q, n_k, w_sink, w_near, lo, hi)
+
+
 def support_size(i_q, n_q, n_k, w_sink, w_near, h_global, h_total):
     """|A_h(i_q)|: the number of distinct visible keys of one query."""
     return sum(b - a for a, b in visible_intervals(i_q, n_q, n_k, w_sink, w_near, h_global, h_total))
 
 
 def support_sizes(n_q, n_k, w_sink, w_near, h_global, h_total):
-    """|A_h(i_q)| for every query i_q = 0..N_q-1 as an int64 array.
+    """|A_h(i_q)| for every query i_q = 0..N_q-1 of the default pattern as an int64 array."""
+    lo, hi = long_window_bounds(n_k, w_sink, w_near, h_global, h_total)
+    return support_sizes_bounds(n_q, n_k, w_sink, w_near, lo, hi)
+
+
+def support_sizes_bounds(n_q, n_k, sink, near, lo, hi):
+    """|A(i_q)| for every query i_q = 0..N_q-1 and window bounds (sink, near,
+    lo, hi) with lo >= near, as an int64 array.
 
     Computed per query from the three windows' key runs with inclusion-exclusion
     over their pairwise overlaps (the near and long runs never overlap because
-    lo >= w_near; sink may overlap either).
+    lo >= near; sink may overlap either).
     """
+    if lo < near:
+        raise ValueError("the long-range window starts after the near window (gap >= 0)")
     iq = np.arange(n_q, dtype=np.int64)
     c = iq + (n_k - n_q)
-    lo, hi = long_window_bounds(n_k, w_sink, w_near, h_global, h_total)
 
     def run(a, b):
         a = np.maximum(a, 0)
         b = np.minimum(b, c + 1)
         return a, np.maximum(b, a)
 
-    na, nb = run(c - w_near + 1, c + 1)
-    sa, sb = run(np.zeros_like(c), np.minimum(w_sink, c + 1))
+    na, nb = run(c - near + 1, c + 1)
+    sa, sb = run(np.zeros_like(c), np.minimum(sink, c + 1))
     fa, fb = run(c - hi + 1, c - lo + 1)
 
     def overlap(a1, b1, a2, b2):
@@ -150,5 +206,5 @@ def support_sizes(n_q, n_k, w_sink, w_near, h_global, h_total):
 
     total = (nb - na) + (sb - sa) + (fb - fa)
     total -= overlap(na, nb, sa, sb) + overlap(fa, fb, sa, sb) + overlap(na, nb, fa, fb)
-    # A triple overlap would need near and long to overlap, which lo >= w_near forbids.
+    # A triple overlap would need near and long to overlap, which lo >= near forbids.
     return total

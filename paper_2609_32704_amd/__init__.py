@@ -10,11 +10,20 @@ the helpers below wrap them for torch tensors:
 
 * ``make_params`` / ``make_decode_params`` -- fill the ABI structs
 * ``Schedule``  -- sizes, allocates and builds the block schedule (cowa_schedule)
-* ``fwd``       -- cowa_fwd: O and LSE
-* ``bwd``       -- cowa_bwd: dQ, dK, dV
+* ``fwd`` / ``fwd_varlen`` -- cowa_fwd: O and LSE (fixed lengths / ragged batch)
+* ``bwd`` / ``bwd_varlen`` -- cowa_bwd: dQ, dK, dV
 * ``decode``    -- cowa_decode: one decoding step over a KV cache
-* ``attention`` -- differentiable attention (torch.autograd.Function over
-                   cowa_fwd and cowa_bwd)
+* ``attention`` / ``attention_varlen`` -- differentiable attention
+                   (torch.autograd.Function over cowa_fwd and cowa_bwd)
+
+Windows: by default every call uses the paper's default rule (shared sink and
+near windows, complementary long-range windows from the global KV-head index).
+``windows=[(sink, near, gap, width), ...]`` (one tuple per local KV head)
+gives explicit per-head windows instead (Sec. 2.1 four-tuple interface).
+
+Ragged batches (``*_varlen``): tensors are packed head-major, Q [H_q, N_q, d]
+and K, V [H_k, N_k, d], sequence b owning rows cu_seqlens[b] .. cu_seqlens[b+1]
+with its queries aligned to the end of its keys.
 """
 
 import math
@@ -23,8 +32,8 @@ from . import _abi
 from ._abi import (CowaError, COWA_BF16, COWA_FP32, cowa_version, cowa_last_error, cowa_windows,  # noqa: F401
                    cowa_schedule_size)
 
-__all__ = ["CowaError", "make_params", "make_decode_params", "Schedule", "fwd", "bwd", "decode", "windows",
-           "attention", "cowa_version"]
+__all__ = ["CowaError", "make_params", "make_decode_params", "Schedule", "fwd", "bwd", "fwd_varlen", "bwd_varlen",
+           "decode", "windows", "attention", "attention_varlen", "cowa_version"]
 
 
 def _torch():
@@ -41,8 +50,26 @@ def _dtype_code(dtype):
     raise ValueError(f"unsupported dtype {dtype}; use torch.bfloat16 or torch.float32")
 
 
+def _host_ints(x, name):
+    """A list of Python ints from a list, tuple, numpy array or torch tensor
+    (a device tensor is copied to the host)."""
+    try:
+        import torch
+        if isinstance(x, torch.Tensor):
+            x = x.detach().cpu().tolist()
+    except ImportError:
+        pass
+    vals = [int(v) for v in (x.tolist() if hasattr(x, "tolist") else x)]
+    if not vals:
+        raise ValueError(f"{name} must have at least one entry")
+    return vals
+
+
 def make_params(batch, n_q, n_k, h_q, h_k, head_dim, w_sink, w_near, tile_q, tile_k, softmax_scale=None,
-                dtype=COWA_BF16, h_k_total=None, h_k_offset=0):
+                dtype=COWA_BF16, h_k_total=None, h_k_offset=0, windows=None, cu_seqlens_q=None, cu_seqlens_k=None):
+    """cowa_params.  windows: None or h_k tuples (sink, near, gap, width).
+    cu_seqlens_q/k: None (fixed lengths) or batch + 1 cumulative lengths of a
+    ragged batch, whose n_q/n_k are then the packed totals."""
     p = _abi.cowa_params()
     p.batch, p.n_q, p.n_k, p.h_q, p.h_k, p.head_dim = batch, n_q, n_k, h_q, h_k, head_dim
     p.w_sink, p.w_near = w_sink, w_near
@@ -51,11 +78,28 @@ def make_params(batch, n_q, n_k, h_q, h_k, head_dim, w_sink, w_near, tile_q, til
     p.tile_q, p.tile_k = tile_q, tile_k
     p.softmax_scale = 1.0 / math.sqrt(head_dim) if softmax_scale is None else softmax_scale
     p.dtype = dtype
+    keep = []
+    if windows is not None:
+        if len(windows) != h_k:
+            raise ValueError(f"windows has {len(windows)} tuples, expected one per local KV head ({h_k})")
+        arr = _abi.window_array(windows)
+        keep.append(arr)
+        p.windows = arr
+    if (cu_seqlens_q is None) != (cu_seqlens_k is None):
+        raise ValueError("cu_seqlens_q and cu_seqlens_k must both be given or both be None")
+    if cu_seqlens_q is not None:
+        cq, ck = _host_ints(cu_seqlens_q, "cu_seqlens_q"), _host_ints(cu_seqlens_k, "cu_seqlens_k")
+        if len(cq) != batch + 1 or len(ck) != batch + 1:
+            raise ValueError(f"cu_seqlens must have batch + 1 = {batch + 1} entries")
+        aq, ak = _abi.int32_array(cq), _abi.int32_array(ck)
+        keep += [aq, ak]
+        p.cu_seqlens_q, p.cu_seqlens_k = aq, ak
+    p._keep = keep
     return p
 
 
 def make_decode_params(batch, h_q, h_k, head_dim, n_max, w_sink, w_near, softmax_scale=None, h_k_total=None,
-                       h_k_offset=0, split_keys=0, dtype=COWA_BF16):
+                       h_k_offset=0, split_keys=0, dtype=COWA_BF16, windows=None):
     p = _abi.cowa_decode_params()
     p.batch, p.h_q, p.h_k, p.head_dim, p.n_max = batch, h_q, h_k, head_dim, n_max
     p.w_sink, p.w_near = w_sink, w_near
@@ -64,6 +108,13 @@ def make_decode_params(batch, h_q, h_k, head_dim, n_max, w_sink, w_near, softmax
     p.split_keys = split_keys
     p.softmax_scale = 1.0 / math.sqrt(head_dim) if softmax_scale is None else softmax_scale
     p.dtype = dtype
+    p._keep = []
+    if windows is not None:
+        if len(windows) != h_k:
+            raise ValueError(f"windows has {len(windows)} tuples, expected one per local KV head ({h_k})")
+        arr = _abi.window_array(windows)
+        p._keep.append(arr)
+        p.windows = arr
     return p
 
 
@@ -84,6 +135,7 @@ class Schedule:
 
     def __init__(self, params, device="cuda", stream=None, build=True):
         torch = _torch()
+        self.params = params  # its host arrays back the pointer fields of self.s.p
         self.s = cowa_schedule_size(params)
         self.buf = torch.empty(max(int(self.s.bytes), 256), dtype=torch.uint8, device=device)
         self.s.buf = self.buf.data_ptr()
@@ -145,40 +197,66 @@ def _dims(q, k, name_q="q", name_k="k"):
     return bsz, h_q, n_q, d, k.shape[1], k.shape[2]
 
 
-def fwd(q, k, v, w_sink, w_near, tile_q, tile_k, softmax_scale=None, h_k_total=None, h_k_offset=0, schedule=None,
-        out=None, lse=None, stream=None):
-    """cowa_fwd.  q [B,H_q,N_q,d], k/v [B,H_k,N_k,d] (bf16 or fp32, contiguous).
-    Returns (o, lse).  ``schedule`` may be a prebuilt Schedule for these shapes."""
+def _dims_varlen(q, k, cu_seqlens_q, cu_seqlens_k):
+    """(B, H_q, N_q, d, H_k, N_k) of packed q [H_q,N_q,d], k [H_k,N_k,d] and
+    the host cumulative lengths."""
     torch = _torch()
-    bsz, h_q, n_q, d, h_k, n_k = _dims(q, k)
-    _validate([(q, "q", q.dtype, (bsz, h_q, n_q, d)), (k, "k", q.dtype, (bsz, h_k, n_k, d)),
-               (v, "v", q.dtype, (bsz, h_k, n_k, d)), (out, "out", q.dtype, (bsz, h_q, n_q, d)),
-               (lse, "lse", torch.float32, (bsz, h_q, n_q))])
-    p = make_params(bsz, n_q, n_k, h_q, h_k, d, w_sink, w_near, tile_q, tile_k, softmax_scale,
-                    _dtype_code(q.dtype), h_k_total, h_k_offset)
+    for t, n in ((q, "q"), (k, "k")):
+        if not isinstance(t, torch.Tensor) or t.dim() != 3:
+            raise ValueError(f"{n} must be a 3-d packed tensor [H, N_total, d]")
+    h_q, n_q, d = q.shape
+    h_k, n_k = k.shape[0], k.shape[1]
+    if k.shape[2] != d:
+        raise ValueError(f"k has shape {tuple(k.shape)}; expected [H_k, N_k, d={d}]")
+    cq, ck = _host_ints(cu_seqlens_q, "cu_seqlens_q"), _host_ints(cu_seqlens_k, "cu_seqlens_k")
+    if len(cq) != len(ck):
+        raise ValueError("cu_seqlens_q and cu_seqlens_k must have the same length")
+    if cq[-1] != n_q or ck[-1] != n_k:
+        raise ValueError(f"cu_seqlens end at ({cq[-1]}, {ck[-1]}) but q and k hold ({n_q}, {n_k}) rows")
+    return len(cq) - 1, h_q, n_q, d, h_k, n_k, cq, ck
+
+
+def _fwd(p, q, k, v, qs, ks, ls, schedule, out, lse, stream):
+    torch = _torch()
+    _validate([(q, "q", q.dtype, qs), (k, "k", q.dtype, ks), (v, "v", q.dtype, ks), (out, "out", q.dtype, qs),
+               (lse, "lse", torch.float32, ls)])
     if schedule is None:
         schedule = Schedule(p, q.device, stream)
     if out is None:
         out = torch.empty_like(q)
     if lse is None:
-        lse = torch.empty((bsz, h_q, n_q), dtype=torch.float32, device=q.device)
+        lse = torch.empty(ls, dtype=torch.float32, device=q.device)
     _abi.cowa_fwd(p, schedule.s, q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
                   _stream(stream))
     return out, lse
 
 
-def bwd(q, k, v, o, lse, do, w_sink, w_near, tile_q, tile_k, softmax_scale=None, h_k_total=None, h_k_offset=0,
-        schedule=None, workspace=None, dq=None, dk=None, dv=None, stream=None):
-    """cowa_bwd.  Returns (dq, dk, dv) for bf16 inputs."""
-    torch = _torch()
+def fwd(q, k, v, w_sink, w_near, tile_q, tile_k, softmax_scale=None, h_k_total=None, h_k_offset=0, schedule=None,
+        out=None, lse=None, stream=None, windows=None):
+    """cowa_fwd.  q [B,H_q,N_q,d], k/v [B,H_k,N_k,d] (bf16 or fp32, contiguous).
+    Returns (o, lse).  ``schedule`` may be a prebuilt Schedule for these shapes."""
     bsz, h_q, n_q, d, h_k, n_k = _dims(q, k)
-    qs, ks = (bsz, h_q, n_q, d), (bsz, h_k, n_k, d)
+    p = make_params(bsz, n_q, n_k, h_q, h_k, d, w_sink, w_near, tile_q, tile_k, softmax_scale,
+                    _dtype_code(q.dtype), h_k_total, h_k_offset, windows)
+    return _fwd(p, q, k, v, (bsz, h_q, n_q, d), (bsz, h_k, n_k, d), (bsz, h_q, n_q), schedule, out, lse, stream)
+
+
+def fwd_varlen(q, k, v, cu_seqlens_q, cu_seqlens_k, w_sink, w_near, tile_q, tile_k, softmax_scale=None,
+               h_k_total=None, h_k_offset=0, schedule=None, out=None, lse=None, stream=None, windows=None):
+    """cowa_fwd on a ragged batch.  q [H_q,N_q,d], k/v [H_k,N_k,d] packed;
+    cu_seqlens_* hold batch + 1 cumulative lengths.  Returns (o, lse [H_q,N_q])."""
+    bsz, h_q, n_q, d, h_k, n_k, cq, ck = _dims_varlen(q, k, cu_seqlens_q, cu_seqlens_k)
+    p = make_params(bsz, n_q, n_k, h_q, h_k, d, w_sink, w_near, tile_q, tile_k, softmax_scale,
+                    _dtype_code(q.dtype), h_k_total, h_k_offset, windows, cq, ck)
+    return _fwd(p, q, k, v, (h_q, n_q, d), (h_k, n_k, d), (h_q, n_q), schedule, out, lse, stream)
+
+
+def _bwd(p, q, k, v, o, lse, do, qs, ks, ls, schedule, workspace, dq, dk, dv, stream):
+    torch = _torch()
     _validate([(q, "q", q.dtype, qs), (k, "k", q.dtype, ks), (v, "v", q.dtype, ks), (o, "o", q.dtype, qs),
-               (do, "do", q.dtype, qs), (lse, "lse", torch.float32, (bsz, h_q, n_q)), (dq, "dq", q.dtype, qs),
+               (do, "do", q.dtype, qs), (lse, "lse", torch.float32, ls), (dq, "dq", q.dtype, qs),
                (dk, "dk", q.dtype, ks), (dv, "dv", q.dtype, ks),
                (workspace, "workspace", torch.uint8, (None if workspace is None else workspace.numel(),))])
-    p = make_params(bsz, n_q, n_k, h_q, h_k, d, w_sink, w_near, tile_q, tile_k, softmax_scale,
-                    _dtype_code(q.dtype), h_k_total, h_k_offset)
     need = _abi.cowa_bwd_workspace_size(p)
     if workspace is not None and workspace.numel() < need:
         raise ValueError(f"workspace has {workspace.numel()} bytes, the backward needs {need}")
@@ -195,8 +273,29 @@ def bwd(q, k, v, o, lse, do, w_sink, w_near, tile_q, tile_k, softmax_scale=None,
     return dq, dk, dv
 
 
+def bwd(q, k, v, o, lse, do, w_sink, w_near, tile_q, tile_k, softmax_scale=None, h_k_total=None, h_k_offset=0,
+        schedule=None, workspace=None, dq=None, dk=None, dv=None, stream=None, windows=None):
+    """cowa_bwd.  Returns (dq, dk, dv) for bf16 inputs."""
+    bsz, h_q, n_q, d, h_k, n_k = _dims(q, k)
+    p = make_params(bsz, n_q, n_k, h_q, h_k, d, w_sink, w_near, tile_q, tile_k, softmax_scale,
+                    _dtype_code(q.dtype), h_k_total, h_k_offset, windows)
+    return _bwd(p, q, k, v, o, lse, do, (bsz, h_q, n_q, d), (bsz, h_k, n_k, d), (bsz, h_q, n_q), schedule,
+                workspace, dq, dk, dv, stream)
+
+
+def bwd_varlen(q, k, v, o, lse, do, cu_seqlens_q, cu_seqlens_k, w_sink, w_near, tile_q, tile_k,
+               softmax_scale=None, h_k_total=None, h_k_offset=0, schedule=None, workspace=None, dq=None, dk=None,
+               dv=None, stream=None, windows=None):
+    """cowa_bwd on a ragged batch (packed tensors as in fwd_varlen)."""
+    bsz, h_q, n_q, d, h_k, n_k, cq, ck = _dims_varlen(q, k, cu_seqlens_q, cu_seqlens_k)
+    p = make_params(bsz, n_q, n_k, h_q, h_k, d, w_sink, w_near, tile_q, tile_k, softmax_scale,
+                    _dtype_code(q.dtype), h_k_total, h_k_offset, windows, cq, ck)
+    return _bwd(p, q, k, v, o, lse, do, (h_q, n_q, d), (h_k, n_k, d), (h_q, n_q), schedule, workspace, dq, dk, dv,
+                stream)
+
+
 def decode(q, k_cache, v_cache, seqlens_k, w_sink, w_near, softmax_scale=None, h_k_total=None, h_k_offset=0,
-           split_keys=0, workspace=None, out=None, lse=None, stream=None):
+           split_keys=0, workspace=None, out=None, lse=None, stream=None, windows=None):
     """cowa_decode.  q [B,H_q,d], caches [B,H_k,n_max,d] bf16, seqlens_k int32 [B]
     on the device.  Returns (o [B,H_q,d], lse [B,H_q])."""
     torch = _torch()
@@ -212,7 +311,7 @@ def decode(q, k_cache, v_cache, seqlens_k, w_sink, w_near, softmax_scale=None, h
                (lse, "lse", torch.float32, (bsz, h_q)),
                (workspace, "workspace", torch.uint8, (None if workspace is None else workspace.numel(),))])
     p = make_decode_params(bsz, h_q, h_k, d, n_max, w_sink, w_near, softmax_scale, h_k_total, h_k_offset,
-                           split_keys, _dtype_code(q.dtype))
+                           split_keys, _dtype_code(q.dtype), windows)
     need = _abi.cowa_decode_workspace_size(p)
     if workspace is not None and workspace.numel() < need:
         raise ValueError(f"workspace has {workspace.numel()} bytes, decoding needs {need}")
@@ -229,7 +328,10 @@ def decode(q, k_cache, v_cache, seqlens_k, w_sink, w_near, softmax_scale=None, h
 
 class _Attention:
     """torch.autograd.Function around cowa_fwd / cowa_bwd (built lazily so that
-    importing the package does not import torch)."""
+    importing the package does not import torch).  The function takes the
+    tensors and one ``cfg`` tuple: (w_sink, w_near, tile_q, tile_k,
+    softmax_scale, h_k_total, h_k_offset, windows, cu_seqlens_q, cu_seqlens_k),
+    the last two None for fixed lengths."""
     fn = None
 
     @classmethod
@@ -239,18 +341,26 @@ class _Attention:
 
             class CowaAttentionFn(torch.autograd.Function):
                 @staticmethod
-                def forward(ctx, q, k, v, w_sink, w_near, tile_q, tile_k, softmax_scale, h_k_total, h_k_offset):
+                def forward(ctx, q, k, v, cfg):
                     q, k, v = q.contiguous(), k.contiguous(), v.contiguous()
-                    p = make_params(q.shape[0], q.shape[2], k.shape[2], q.shape[1], k.shape[1], q.shape[3],
-                                    w_sink, w_near, tile_q, tile_k, softmax_scale, _dtype_code(q.dtype),
-                                    h_k_total, h_k_offset)
-                    sched = Schedule(p, q.device)
-                    o, lse = fwd(q, k, v, w_sink, w_near, tile_q, tile_k, softmax_scale, h_k_total, h_k_offset,
-                                 schedule=sched)
+                    w_sink, w_near, tq, tk, scale, h_tot, h_off, wins, cq, ck = cfg
+                    if cq is None:
+                        sched_p = make_params(q.shape[0], q.shape[2], k.shape[2], q.shape[1], k.shape[1], q.shape[3],
+                                              w_sink, w_near, tq, tk, scale, _dtype_code(q.dtype), h_tot, h_off, wins)
+                        sched = Schedule(sched_p, q.device)
+                        o, lse = fwd(q, k, v, w_sink, w_near, tq, tk, scale, h_tot, h_off, schedule=sched,
+                                     windows=wins)
+                    else:
+                        sched_p = make_params(len(cq) - 1, q.shape[1], k.shape[1], q.shape[0], k.shape[0],
+                                              q.shape[2], w_sink, w_near, tq, tk, scale, _dtype_code(q.dtype), h_tot,
+                                              h_off, wins, cq, ck)
+                        sched = Schedule(sched_p, q.device)
+                        o, lse = fwd_varlen(q, k, v, cq, ck, w_sink, w_near, tq, tk, scale, h_tot, h_off,
+                                            schedule=sched, windows=wins)
                     ctx.save_for_backward(q, k, v, o, lse)
                     ctx.mark_non_differentiable(lse)
                     ctx.set_materialize_grads(False)
-                    ctx.cfg = (w_sink, w_near, tile_q, tile_k, softmax_scale, h_k_total, h_k_offset)
+                    ctx.cfg = cfg
                     ctx.sched = sched
                     return o, lse
 
@@ -258,22 +368,39 @@ class _Attention:
                 def backward(ctx, d_o, d_lse):
                     q, k, v, o, lse = ctx.saved_tensors
                     if d_o is None:
-                        return (None,) * 10
-                    w_sink, w_near, tile_q, tile_k, scale, h_k_total, h_k_offset = ctx.cfg
-                    dq, dk, dv = bwd(q, k, v, o, lse, d_o.contiguous(), w_sink, w_near, tile_q, tile_k, scale,
-                                     h_k_total, h_k_offset, schedule=ctx.sched)
-                    return dq, dk, dv, None, None, None, None, None, None, None
+                        return None, None, None, None
+                    w_sink, w_near, tq, tk, scale, h_tot, h_off, wins, cq, ck = ctx.cfg
+                    if cq is None:
+                        dq, dk, dv = bwd(q, k, v, o, lse, d_o.contiguous(), w_sink, w_near, tq, tk, scale, h_tot,
+                                         h_off, schedule=ctx.sched, windows=wins)
+                    else:
+                        dq, dk, dv = bwd_varlen(q, k, v, o, lse, d_o.contiguous(), cq, ck, w_sink, w_near, tq, tk,
+                                                scale, h_tot, h_off, schedule=ctx.sched, windows=wins)
+                    return dq, dk, dv, None
 
             cls.fn = CowaAttentionFn
         return cls.fn
 
 
 def attention(q, k, v, w_sink, w_near, tile_q=128, tile_k=128, softmax_scale=None, h_k_total=None, h_k_offset=0,
-              return_lse=False):
+              return_lse=False, windows=None):
     """Differentiable CoWA attention (torch autograd): the forward runs cowa_fwd
     and saves O and LSE; the backward runs cowa_bwd (deterministic: the same
     inputs give bitwise the same gradients).  q [B,H_q,N_q,d], k/v
     [B,H_k,N_k,d], bf16 for the backward.  Returns O (and LSE, treated as a
     non-differentiable output, if return_lse)."""
-    o, lse = _Attention.get().apply(q, k, v, w_sink, w_near, tile_q, tile_k, softmax_scale, h_k_total, h_k_offset)
+    cfg = (w_sink, w_near, tile_q, tile_k, softmax_scale, h_k_total, h_k_offset,
+           None if windows is None else [tuple(w) for w in windows], None, None)
+    o, lse = _Attention.get().apply(q, k, v, cfg)
+    return (o, lse) if return_lse else o
+
+
+def attention_varlen(q, k, v, cu_seqlens_q, cu_seqlens_k, w_sink, w_near, tile_q=128, tile_k=128,
+                     softmax_scale=None, h_k_total=None, h_k_offset=0, return_lse=False, windows=None):
+    """attention() on a ragged batch: q [H_q,N_q,d], k/v [H_k,N_k,d] packed,
+    cu_seqlens_* with batch + 1 cumulative lengths."""
+    cfg = (w_sink, w_near, tile_q, tile_k, softmax_scale, h_k_total, h_k_offset,
+           None if windows is None else [tuple(w) for w in windows],
+           _host_ints(cu_seqlens_q, "cu_seqlens_q"), _host_ints(cu_seqlens_k, "cu_seqlens_k"))
+    o, lse = _Attention.get().apply(q, k, v, cfg)
     return (o, lse) if return_lse else o

@@ -31,11 +31,15 @@ class cowa_window(ctypes.Structure):
 
 
 class cowa_params(ctypes.Structure):
+    """The C struct.  The pointer fields reference host arrays that the
+    Python object keeps alive in ``_keep`` (set by make_params)."""
     _fields_ = [("batch", ctypes.c_int32), ("n_q", ctypes.c_int32), ("n_k", ctypes.c_int32),
                 ("h_q", ctypes.c_int32), ("h_k", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("w_sink", ctypes.c_int32), ("w_near", ctypes.c_int32), ("h_k_total", ctypes.c_int32),
                 ("h_k_offset", ctypes.c_int32), ("tile_q", ctypes.c_int32), ("tile_k", ctypes.c_int32),
-                ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32)]
+                ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32),
+                ("windows", ctypes.POINTER(cowa_window)), ("cu_seqlens_q", ctypes.POINTER(ctypes.c_int32)),
+                ("cu_seqlens_k", ctypes.POINTER(ctypes.c_int32))]
 
 
 class cowa_schedule_t(ctypes.Structure):
@@ -43,6 +47,9 @@ class cowa_schedule_t(ctypes.Structure):
                 ("max_row", ctypes.c_int32), ("max_col", ctypes.c_int32), ("nnz", ctypes.c_int64),
                 ("off_fwd_row_ptr", ctypes.c_size_t), ("off_bwd_col_ptr", ctypes.c_size_t),
                 ("off_fwd_ent", ctypes.c_size_t), ("off_bwd_ent", ctypes.c_size_t),
+                ("off_windows", ctypes.c_size_t), ("off_seqs", ctypes.c_size_t),
+                ("off_qt_seq", ctypes.c_size_t), ("off_kt_seq", ctypes.c_size_t),
+                ("max_qt", ctypes.c_int32), ("max_kt", ctypes.c_int32), ("digest", ctypes.c_uint64),
                 ("bytes", ctypes.c_size_t), ("buf", ctypes.c_void_p)]
 
 
@@ -50,7 +57,20 @@ class cowa_decode_params(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("h_q", ctypes.c_int32), ("h_k", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("n_max", ctypes.c_int32), ("w_sink", ctypes.c_int32),
                 ("w_near", ctypes.c_int32), ("h_k_total", ctypes.c_int32), ("h_k_offset", ctypes.c_int32),
-                ("split_keys", ctypes.c_int32), ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32)]
+                ("split_keys", ctypes.c_int32), ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32),
+                ("windows", ctypes.POINTER(cowa_window))]
+
+
+def window_array(tuples):
+    """A C array of cowa_window from (sink, near, gap, width) tuples."""
+    arr = (cowa_window * len(tuples))()
+    for x, t in enumerate(tuples):
+        arr[x].sink, arr[x].near, arr[x].gap, arr[x].width = (int(v) for v in t)
+    return arr
+
+
+def int32_array(values):
+    return (ctypes.c_int32 * len(values))(*[int(v) for v in values])
 
 
 _P = ctypes.POINTER

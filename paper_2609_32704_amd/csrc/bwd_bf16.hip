@@ -27,6 +27,7 @@
 #include "internal.h"
 #include "window_rule.h"
 #include "mfma_tiles.h"
+#include "work_item.h"
 
 namespace cowa {
 namespace {
@@ -97,28 +98,30 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
 
   // clusters of 32 consecutive KV blocks of one KV head share an XCD's L2;
   // first blocks (the sink, with the longest query lists) first
-  const WorkItem wi = cluster_item(blockIdx.x, sv.n_kt, 1, p.batch * p.h_k, 32, false);
-  const int j = wi.row;
-  const int hk = wi.unit % p.h_k;
-  const int b = wi.unit / p.h_k;
+  const WorkItem wi = cluster_item(blockIdx.x, sv.n_kt, 1, grid_units(p, sv), 32, false);
+  int hk;
+  const SeqCtx sc = seq_ctx(p, sv, wi.row, wi.unit, false, hk);
+  const int j = sc.tile;
   const int G = p.h_q / p.h_k;
-  const Geo32 g = geo32(make_geo(p.n_q, p.n_k, p.w_sink, p.w_near, p.tile_q, BK, p.h_k_offset + hk, p.h_k_total));
+  const Geo32 g = sc.g;
+  const int n_q = sc.n_q, n_k = sc.n_k;
 
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int lr = lane & 15, lg = lane >> 4;
   const int64_t k_first = (int64_t)j * BK;
-  const __bf16* kbase = k + ((int64_t)b * p.h_k + hk) * p.n_k * D;
-  const __bf16* vbase = v + ((int64_t)b * p.h_k + hk) * p.n_k * D;
+  const int64_t kv_row0 = sc.k0 + (int64_t)hk * sc.kh;
+  const __bf16* kbase = k + kv_row0 * D;
+  const __bf16* vbase = v + kv_row0 * D;
 
   // The steps: every QO head of the group x every QO block of I(j) x 64-row
   // sub-blocks.  Full blocks are taken first, then partial ones, so that each
   // of the two step loops below is straight-line code (the partial loop adds
   // the element mask).  The column's entries are split once into two lists in
   // LDS: full entries from the front, partial entries from the back.
-  const int col = hk * sv.n_kt + j;
+  const int col = sc.sched;
   const int e0 = sv.bwd_col_ptr[col], e1 = sv.bwd_col_ptr[col + 1];
   const int n_ent = e1 - e0;
-  const int cap = sv.n_qt;  // list capacity (entries of one column)
+  const int cap = sv.max_qt;  // list capacity (entries of one column)
   uint32_t* list = reinterpret_cast<uint32_t*>(smem + C::MAIN_BYTES);
   int n_full = 0;
   for (int c0 = 0; c0 < n_ent; c0 += 64) {  // every wave builds the same counts; wave 0 writes
@@ -196,10 +199,10 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
   auto stage_src = [&](uint32_t ent, int hh, int sub) -> StageSrc {
     hh = hh < G ? hh : G - 1;
     const int q0 = (int)(ent >> 1) * p.tile_q + sub * C::BQ;
-    const int64_t row_base = ((int64_t)b * p.h_q + hk * G + hh) * p.n_q;
-    const uint32_t bytes = (uint32_t)(p.n_q - q0) * D * 2;
+    const int64_t row_base = sc.q0 + (int64_t)(hk * G + hh) * sc.qh;
+    const uint32_t bytes = (uint32_t)(n_q - q0) * D * 2;
     const int r = q0 + lane;
-    const int rc = r < p.n_q ? r : p.n_q - 1;
+    const int rc = r < n_q ? r : n_q - 1;
     return StageSrc{(row_base + q0) * D * 2, bytes, ((wave & 1) ? dsum : lse) + row_base + rc};
   };
   auto stage_piece = [&](const StageSrc& src, int n, int slot) {
@@ -236,7 +239,7 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
 #pragma unroll
   for (int nt = 0; nt < C::NTK; ++nt) {
     int64_t kp = k_first + wave * C::NKW + nt * 16 + lr;
-    if (kp >= p.n_k) kp = p.n_k - 1;  // masked: such keys are in partial blocks only
+    if (kp >= n_k) kp = n_k - 1;  // masked: such keys are in partial blocks only
 #pragma unroll
     for (int ks = 0; ks < C::KSD; ++ks) {
       kf[nt][ks] = *reinterpret_cast<const bf16x8*>(kbase + kp * D + ks * 32 + 8 * lg);
@@ -430,12 +433,12 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
         tv[key * (D + 8) + d] = (__bf16)dva[md][nt][rr];
       }
   __syncthreads();
-  __bf16* dkb = dk + ((int64_t)b * p.h_k + hk) * p.n_k * D;
-  __bf16* dvb = dv + ((int64_t)b * p.h_k + hk) * p.n_k * D;
+  __bf16* dkb = dk + kv_row0 * D;
+  __bf16* dvb = dv + kv_row0 * D;
   for (int x = tid; x < BK * (D / 8); x += blockDim.x) {
     const int key = x / (D / 8), ch = x % (D / 8);
     const int64_t kp = k_first + key;
-    if (kp < p.n_k) {
+    if (kp < n_k) {
       *reinterpret_cast<uint4*>(dkb + kp * D + ch * 8) = *reinterpret_cast<const uint4*>(tk + key * (D + 8) + ch * 8);
       *reinterpret_cast<uint4*>(dvb + kp * D + ch * 8) = *reinterpret_cast<const uint4*>(tv + key * (D + 8) + ch * 8);
     }
@@ -448,14 +451,14 @@ hipError_t launch_main(const cowa_params& p, const SchedView& sv, const void* q,
                        hipStream_t stream) {
   using C = BwdCfg<D, BK, NW>;
   static_assert(C::OUT_BYTES <= C::LDS_MAX && C::MAIN_BYTES < C::LDS_MAX, "LDS budget");
-  if (sv.n_qt > C::max_qblocks()) return hipErrorInvalidValue;
+  if (sv.max_qt > C::max_qblocks()) return hipErrorInvalidValue;
   auto kern = bwd_main<D, BK, NW>;
   {
     const hipError_t err = allow_lds(reinterpret_cast<const void*>(kern), C::LDS_MAX);
     if (err != hipSuccess) return err;
   }
-  const unsigned blocks = (unsigned)sv.n_kt * p.h_k * p.batch;
-  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * NW), C::lds_bytes(sv.n_qt), stream, p, sv,
+  const unsigned blocks = (unsigned)sv.n_kt * p.h_k * (sv.ragged ? 1 : p.batch);
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * NW), C::lds_bytes(sv.max_qt), stream, p, sv,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), static_cast<const __bf16*>(v),
                      static_cast<const __bf16*>(d_o), lse, dsum, static_cast<__bf16*>(dk),
                      static_cast<__bf16*>(dv));
@@ -506,9 +509,10 @@ __global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, S
   const int G = p.h_q / p.h_k;
   // rows of 16 QO blocks x the head groups of one KV head share an XCD's L2;
   // latest (longest) QO blocks first
-  const WorkItem wi = cluster_item(blockIdx.x, sv.n_qt, G / hpw, p.batch * p.h_k, 16, true);
-  const int i = wi.row, b = wi.unit / p.h_k;
-  const int hk = wi.unit % p.h_k;
+  const WorkItem wi = cluster_item(blockIdx.x, sv.n_qt, G / hpw, grid_units(p, sv), 16, true);
+  int hk;
+  const SeqCtx sc = seq_ctx(p, sv, wi.row, wi.unit, true, hk);
+  const int i = sc.tile;
   const int hgi = hk * (G / hpw) + wi.group;
   const int h0 = hgi * hpw;
 
@@ -516,17 +520,18 @@ __global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, S
   const int lr = lane & 15, lg = lane >> 4;
   const int h = h0 + wave / C::WPH;
   const int q_first = i * BQ + (wave % C::WPH) * C::NQW;
-  const Geo32 g = geo32(make_geo(p.n_q, p.n_k, p.w_sink, p.w_near, BQ, BK, p.h_k_offset + hk, p.h_k_total));
+  const Geo32 g = sc.g;
+  const int n_q = sc.n_q, n_k = sc.n_k;
 
-  const __bf16* kbase = k + ((int64_t)b * p.h_k + hk) * p.n_k * D;
-  const __bf16* vbase = v + ((int64_t)b * p.h_k + hk) * p.n_k * D;
+  const __bf16* kbase = k + (sc.k0 + (int64_t)hk * sc.kh) * D;
+  const __bf16* vbase = v + (sc.k0 + (int64_t)hk * sc.kh) * D;
   const uint32_t smem_base = lds_addr(smem);
 
   // the row's entries, split into full (from the front) and partial (from the back) lists
-  const int r = hk * sv.n_qt + i;
+  const int r = sc.sched;
   const int e0 = sv.fwd_row_ptr[r], e1 = sv.fwd_row_ptr[r + 1];
   const int n_ent = e1 - e0;
-  const int cap = sv.n_kt;
+  const int cap = sv.max_kt;
   uint32_t* list = reinterpret_cast<uint32_t*>(smem + C::MAIN_BYTES);
   int n_full = 0;
   for (int c0 = 0; c0 < n_ent; c0 += 64) {
@@ -551,8 +556,8 @@ __global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, S
   };
   auto stage = [&](uint32_t ent, int buf) {
     const int kf = (int)(ent >> 1) * BK;
-    load_tile_asm_nw<D, BK>(kbase, kf, p.n_k, smem_base + buf * 2 * T::BYTES, wave, nw, lane);
-    load_tile_asm_nw<D, BK>(vbase, kf, p.n_k, smem_base + buf * 2 * T::BYTES + T::BYTES, wave, nw, lane);
+    load_tile_asm_nw<D, BK>(kbase, kf, n_k, smem_base + buf * 2 * T::BYTES, wave, nw, lane);
+    load_tile_asm_nw<D, BK>(vbase, kf, n_k, smem_base + buf * 2 * T::BYTES + T::BYTES, wave, nw, lane);
   };
   __syncthreads();  // the lists are in LDS
   if (n_ent > 0) stage(entry_at(0), 0);
@@ -566,20 +571,20 @@ __global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, S
   const int col0 = ((lane % T::CH) ^ swz<T::CH>(row0)) << 3;
   auto stage_piece = [&](const __bf16* base, int kf, int buf, int n, int isv) {
     int r = kf + n * 4 * RPL + row0;
-    r = r < p.n_k ? r : p.n_k - 1;
+    r = r < n_k ? r : n_k - 1;
     dma16(base + (int64_t)r * D + col0,
           __builtin_amdgcn_readfirstlane(smem_base + buf * 2 * T::BYTES + isv * T::BYTES + (n * 4 + wave) * 1024));
   };
 
   // Q^T and dO^T fragments (B operands): query column nt*16 + lr, d = ks*32 + 8*lg + 0..7;
   // per-query LSE (base 2; a row without keys or past n_q gets +inf, so P = 0) and D
-  const int64_t row_base = ((int64_t)b * p.h_q + h) * p.n_q;
+  const int64_t row_base = sc.q0 + (int64_t)h * sc.qh;
   bf16x8 qf[NTQ][KSD], gf[NTQ][KSD];
   float l2[NTQ], dd[NTQ];
 #pragma unroll
   for (int nt = 0; nt < NTQ; ++nt) {
     const int qp = q_first + nt * 16 + lr;
-    const bool ok = qp < p.n_q;
+    const bool ok = qp < n_q;
     const int64_t row = row_base + (ok ? qp : 0);
 #pragma unroll
     for (int ks = 0; ks < KSD; ++ks) {
@@ -716,7 +721,7 @@ __global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, S
 #pragma unroll
   for (int nt = 0; nt < NTQ; ++nt) {
     const int qp = q_first + nt * 16 + lr;
-    if (qp >= p.n_q) continue;
+    if (qp >= n_q) continue;
     __bf16* drow = dq + (row_base + qp) * D;
 #pragma unroll
     for (int md = 0; md < MTD; ++md) {
@@ -739,8 +744,8 @@ hipError_t launch_dq_w(const cowa_params& p, const SchedView& sv, int hpw, int w
     if (err != hipSuccess) return err;
   }
   const int n_hgroups = p.h_q / hpw;
-  const unsigned blocks = (unsigned)sv.n_qt * n_hgroups * p.batch;
-  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * waves), C::lds_bytes(sv.n_kt), stream, p, sv, hpw,
+  const unsigned blocks = (unsigned)sv.n_qt * n_hgroups * (sv.ragged ? 1 : p.batch);
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * waves), C::lds_bytes(sv.max_kt), stream, p, sv, hpw,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), static_cast<const __bf16*>(v),
                      static_cast<const __bf16*>(d_o), lse, dsum, static_cast<__bf16*>(dq));
   return hipGetLastError();
@@ -750,7 +755,7 @@ template <int D, int BQ, int BK, int NQW = 64>
 hipError_t launch_dq(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
                      const void* d_o, const float* lse, const float* dsum, void* dq, hipStream_t stream) {
   using C = DqCfg<D, BQ, BK, NQW>;
-  if (sv.n_kt > C::max_kblocks()) return hipErrorInvalidValue;
+  if (sv.max_kt > C::max_kblocks()) return hipErrorInvalidValue;
   const int G = p.h_q / p.h_k;
   int hpw = 256 / BQ;  // up to 256 query rows per workgroup
   while (hpw > 1 && G % hpw != 0) hpw >>= 1;
@@ -778,7 +783,7 @@ bool bwd_bf16_supported(int d, int tq, int tk) {
 
 hipError_t launch_bwd_prepare(const cowa_params& p, const void* o, const void* d_o, float* dsum,
                               hipStream_t stream) {
-  const int64_t rows = (int64_t)p.batch * p.h_q * p.n_q;
+  const int64_t rows = q_rows(p);
   const int64_t chunks = rows * (p.head_dim / 8);
   const unsigned blocks = (unsigned)((chunks + 255) / 256);
   if (p.head_dim == 128)

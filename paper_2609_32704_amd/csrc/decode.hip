@@ -24,6 +24,8 @@ constexpr int64_t kTargetPrograms = 1024;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
+constexpr int kHeadsPerLaunch = 32;  // explicit windows travel in the kernel arguments, 32 heads at a time
+
 struct DecArgs {
   const __bf16* q;
   const __bf16* kc;
@@ -35,7 +37,55 @@ struct DecArgs {
   float* part_ml;  // [B][H_q][S][2]
   int32_t batch, h_q, h_k, n_max, w_sink, w_near, h_total, h_offset, splits, split_keys;
   float c;  // softmax_scale * log2(e)
+  int32_t explicit_win;            // windows below (else the default rule from each sequence's N_k)
+  int32_t head_base;               // first local KV head of this launch
+  WinDesc win[kHeadsPerLaunch];    // explicit windows of heads head_base .. head_base + 31
 };
+
+// The visible keys of the decoding query (distance-0 key c = N_k - 1) as up to
+// three ascending, merged key runs [a, b] -- the union of the sink, long-range
+// and near windows of Sec. 2.1 -- computed with scalar selects only (no
+// indexed arrays, which the compiler would place in scratch memory).  Empty
+// runs have a = kNone.
+constexpr int32_t kNone = 0x3fffffff;
+struct Runs3 {
+  int32_t a0, b0, a1, b1, a2, b2;
+};
+__device__ inline void order2(int32_t& a, int32_t& b, int32_t& c, int32_t& d) {  // (a, b) before (c, d)
+  const bool sw = c < a;
+  const int32_t ta = sw ? c : a, tb = sw ? d : b, tc = sw ? a : c, td = sw ? b : d;
+  a = ta; b = tb; c = tc; d = td;
+}
+__device__ inline Runs3 key_runs3(int32_t n_k, int32_t sink, int32_t near, int32_t lo, int32_t hi) {
+  const int32_t c = n_k - 1;
+  Runs3 r;
+  // near: delta in [0, near); sink: keys below sink; long: delta in [lo, hi)
+  r.a0 = near >= 1 ? max(0, c - near + 1) : kNone;
+  r.b0 = near >= 1 ? c : kNone - 1;
+  r.a1 = sink >= 1 ? 0 : kNone;
+  r.b1 = sink >= 1 ? min(sink - 1, c) : kNone - 1;
+  const bool has_long = hi > lo && c - lo >= 0;
+  r.a2 = has_long ? max(0, c - hi + 1) : kNone;
+  r.b2 = has_long ? c - lo : kNone - 1;
+  order2(r.a0, r.b0, r.a1, r.b1);
+  order2(r.a1, r.b1, r.a2, r.b2);
+  order2(r.a0, r.b0, r.a1, r.b1);
+  // merge overlapping or touching runs (an empty run starts at kNone and never merges)
+  if (r.a1 != kNone && r.a1 <= r.b0 + 1) {
+    r.b0 = max(r.b0, r.b1);
+    r.a1 = r.a2; r.b1 = r.b2;
+    r.a2 = kNone; r.b2 = kNone - 1;
+  }
+  if (r.a1 != kNone && r.a1 <= r.b0 + 1) {
+    r.b0 = max(r.b0, r.b1);
+    r.a1 = kNone; r.b1 = kNone - 1;
+  }
+  if (r.a2 != kNone && r.a2 <= r.b1 + 1) {
+    r.b1 = max(r.b1, r.b2);
+    r.a2 = kNone; r.b2 = kNone - 1;
+  }
+  return r;
+}
 
 // Sum over the DC lanes of each lane group (DC = 8 or 16 consecutive lanes,
 // inside one 16-lane DPP row), the result in every lane of the group:
@@ -66,21 +116,25 @@ __global__ void __launch_bounds__(256) decode_split(DecArgs a) {
   __shared__ float sm_m[4][G], sm_l[4][G];
   __shared__ float sm_o[4][G][D];
 
-  const int s = blockIdx.x, hk = blockIdx.y, b = blockIdx.z;
+  const int s = blockIdx.x, hk = a.head_base + blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int kg = lane / DC, dc = lane % DC;
 
   const int32_t n_k = a.seqlens[b];
   const bool valid = n_k >= 1 && n_k <= a.n_max;
-  Ranges runs;
-  runs.n = 0;
-  int32_t total = 0;
+  Runs3 runs{kNone, kNone - 1, kNone, kNone - 1, kNone, kNone - 1};
   if (valid) {
-    int64_t lo, hi;
-    long_bounds(n_k, a.w_sink, a.w_near, (int64_t)a.h_offset + hk, a.h_total, &lo, &hi);
-    runs = decode_key_runs(n_k, a.w_sink, a.w_near, lo, hi);
-    total = ranges_count(runs);
+    WinDesc w;
+    if (a.explicit_win) {
+      w = a.win[blockIdx.y];
+    } else {
+      int64_t lo, hi;
+      long_bounds(n_k, a.w_sink, a.w_near, (int64_t)a.h_offset + hk, a.h_total, &lo, &hi);
+      w = WinDesc{a.w_sink, a.w_near, (int32_t)lo, (int32_t)hi};
+    }
+    runs = key_runs3(n_k, min(w.sink, n_k), min(w.near, n_k), min(w.lo, n_k), min(w.hi, n_k));
   }
+  const int32_t total = (runs.b0 - runs.a0 + 1) + (runs.b1 - runs.a1 + 1) + (runs.b2 - runs.a2 + 1);
   const int32_t v0 = s * a.split_keys;
   const int32_t v1 = min(v0 + a.split_keys, total);
 
@@ -109,13 +163,15 @@ __global__ void __launch_bounds__(256) decode_split(DecArgs a) {
   // runs; each run is streamed as a contiguous key range
   int32_t off = 0;
 #pragma unroll
-  for (int r = 0; r < 3; ++r) {  // unrolled: the run arrays stay in registers
-    if (r >= runs.n) break;
-    const int32_t len = runs.b[r] - runs.a[r] + 1;
+  for (int r = 0; r < 3; ++r) {
+    const int32_t ra = r == 0 ? runs.a0 : r == 1 ? runs.a1 : runs.a2;
+    const int32_t rb = r == 0 ? runs.b0 : r == 1 ? runs.b1 : runs.b2;
+    if (ra == kNone) break;
+    const int32_t len = rb - ra + 1;
     const int32_t lo = max(v0, off), hi = min(v1, off + len);
     off += len;
     if (lo >= hi) continue;
-    const int32_t k_lo = runs.a[r] + (lo - off + len), k_hi = runs.a[r] + (hi - off + len);  // keys [k_lo, k_hi)
+    const int32_t k_lo = ra + (lo - off + len), k_hi = ra + (hi - off + len);  // keys [k_lo, k_hi)
     for (int32_t kb = k_lo; kb < k_hi; kb += STEP * U) {
       uint4 kr[U], vr[U];
       bool ok[U];
@@ -251,16 +307,43 @@ __global__ void __launch_bounds__(256) decode_combine(DecArgs a) {
   if (lane == 0) a.lse[wave] = lv > 0.f ? (mm + __log2f(lv)) * kLn2 : -INFINITY;
 }
 
+// An upper bound of the visible keys of any (sequence, KV head): sink + near +
+// the long-range width, at most n_max.
 int32_t max_visible(const cowa_decode_params& p) {
-  const int64_t span = p.n_max - (int64_t)p.w_sink - p.w_near;
-  const int64_t width = span > 0 ? (span + p.h_k_total - 1) / p.h_k_total : 0;
-  const int64_t v = (int64_t)p.w_sink + p.w_near + width;
+  int64_t v = 0;
+  if (p.windows) {
+    for (int h = 0; h < p.h_k; ++h) {
+      const cowa_window& w = p.windows[h];
+      const int64_t x = (int64_t)w.sink + w.near + w.width;
+      v = x > v ? x : v;
+    }
+  } else {
+    const int64_t span = p.n_max - (int64_t)p.w_sink - p.w_near;
+    const int64_t width = span > 0 ? (span + p.h_k_total - 1) / p.h_k_total : 0;
+    v = (int64_t)p.w_sink + p.w_near + width;
+  }
   return (int32_t)(v < p.n_max ? v : p.n_max);
 }
 
 template <int D, int G>
-hipError_t launch_dg(const DecArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL((decode_split<D, G>), dim3(a.splits, a.h_k, a.batch), dim3(256), 0, stream, a);
+hipError_t launch_dg(DecArgs a, const cowa_window* windows, hipStream_t stream) {
+  if (!windows) {
+    a.explicit_win = 0;
+    a.head_base = 0;
+    hipLaunchKernelGGL((decode_split<D, G>), dim3(a.splits, a.h_k, a.batch), dim3(256), 0, stream, a);
+  } else {
+    a.explicit_win = 1;
+    for (int h0 = 0; h0 < a.h_k; h0 += kHeadsPerLaunch) {
+      const int nh = a.h_k - h0 < kHeadsPerLaunch ? a.h_k - h0 : kHeadsPerLaunch;
+      a.head_base = h0;
+      for (int x = 0; x < nh; ++x) {
+        const cowa_window& w = windows[h0 + x];
+        const int64_t lo = (int64_t)w.near + w.gap, hi = lo + w.width, cap = int64_t(1) << 30;
+        a.win[x] = WinDesc{w.sink, w.near, (int32_t)(lo < cap ? lo : cap), (int32_t)(hi < cap ? hi : cap)};
+      }
+      hipLaunchKernelGGL((decode_split<D, G>), dim3(a.splits, nh, a.batch), dim3(256), 0, stream, a);
+    }
+  }
   const int waves = a.batch * a.h_q;
   hipLaunchKernelGGL(decode_combine<D>, dim3((waves + 3) / 4), dim3(256), 0, stream, a);
   return hipGetLastError();
@@ -317,7 +400,7 @@ hipError_t launch_decode(const cowa_decode_params& p, const void* q, const void*
   a.part_o = static_cast<float*>(ws);
   a.part_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + ((parts * p.head_dim * sizeof(float) + 255) & ~size_t(255)));
   const int G = p.h_q / p.h_k;
-#define COWA_DEC_CASE(D_, G_) if (p.head_dim == D_ && G == G_) return launch_dg<D_, G_>(a, stream);
+#define COWA_DEC_CASE(D_, G_) if (p.head_dim == D_ && G == G_) return launch_dg<D_, G_>(a, p.windows, stream);
   COWA_DEC_CASE(128, 4) COWA_DEC_CASE(128, 1) COWA_DEC_CASE(128, 2) COWA_DEC_CASE(128, 8)
   COWA_DEC_CASE(64, 4) COWA_DEC_CASE(64, 1) COWA_DEC_CASE(64, 2) COWA_DEC_CASE(64, 8)
 #undef COWA_DEC_CASE

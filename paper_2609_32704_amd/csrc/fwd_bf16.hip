@@ -28,6 +28,7 @@
 #include "internal.h"
 #include "window_rule.h"
 #include "mfma_tiles.h"
+#include "work_item.h"
 
 namespace cowa {
 namespace {
@@ -110,9 +111,10 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   const int G = p.h_q / p.h_k;
   // rows of 16 QO blocks x the head groups of one KV head share an XCD's L2;
   // latest (longest) QO blocks first
-  const WorkItem wi = cluster_item(blockIdx.x, sv.n_qt, G / hpw, p.batch * p.h_k, 16, true);
-  const int i = wi.row, b = wi.unit / p.h_k;
-  const int hk = wi.unit % p.h_k;
+  const WorkItem wi = cluster_item(blockIdx.x, sv.n_qt, G / hpw, grid_units(p, sv), 16, true);
+  int hk;
+  const SeqCtx sc = seq_ctx(p, sv, wi.row, wi.unit, true, hk);
+  const int i = sc.tile;
   const int hgi = hk * (G / hpw) + wi.group;
   const int h0 = hgi * hpw;  // first QO head of this workgroup (all in KV group hk)
 
@@ -120,9 +122,10 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   const int l32 = lane & 31, hh = lane >> 5;  // MFMA column and half
   const int hq = h0 + wave / C::WPH;
   const int q_first = i * BQ + (wave % C::WPH) * C::NQW;
-  const Geo32 g = geo32(make_geo(p.n_q, p.n_k, p.w_sink, p.w_near, BQ, BK, p.h_k_offset + hk, p.h_k_total));
-  const __bf16* kbase = k + ((int64_t)b * p.h_k + hk) * p.n_k * D;
-  const __bf16* vbase = v + ((int64_t)b * p.h_k + hk) * p.n_k * D;
+  const Geo32 g = sc.g;
+  const int n_q = sc.n_q, n_k = sc.n_k;
+  const __bf16* kbase = k + (sc.k0 + (int64_t)hk * sc.kh) * D;
+  const __bf16* vbase = v + (sc.k0 + (int64_t)hk * sc.kh) * D;
   const uint32_t smem_base = lds_addr(smem);
 
   // zero the K/V buffers once: key rows past the end of the sequence are not
@@ -130,10 +133,10 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   for (int x = tid; x < C::MAIN_BYTES / 16; x += blockDim.x) reinterpret_cast<u32x4*>(smem)[x] = u32x4{0u, 0u, 0u, 0u};
 
   // the row's entries, split into full (from the front) and partial (from the back) lists
-  const int r = hk * sv.n_qt + i;
+  const int r = sc.sched;
   const int e0 = sv.fwd_row_ptr[r], e1 = sv.fwd_row_ptr[r + 1];
   const int n_ent = e1 - e0;
-  const int cap = sv.n_kt;
+  const int cap = sv.max_kt;
   uint32_t* list = reinterpret_cast<uint32_t*>(smem + C::MAIN_BYTES);
   int n_full = 0;
   for (int c0 = 0; c0 < n_ent; c0 += 64) {
@@ -175,28 +178,28 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   auto stage = [&](const __bf16* base, int t, int buf_off) {
     const int kf = (int)(entry_at(t) >> 1) * BK;
     if constexpr (FULL) {
-      const i32x4 rs = buffer_rsrc(base + (int64_t)kf * D, (uint32_t)(p.n_k - kf) * D * 2);
+      const i32x4 rs = buffer_rsrc(base + (int64_t)kf * D, (uint32_t)(n_k - kf) * D * 2);
       const uint32_t lds0 = smem_base + buf_off + wave * 1024;
 #pragma unroll
       for (int n = 0; n < PPW; ++n) dma16_buf(dma_off[n], rs, lds0 + n * NWF * 1024);
     } else {
-      load_tile_asm_nw<D, BK>(base, kf, p.n_k, smem_base + buf_off, wave, nw, lane);
+      load_tile_asm_nw<D, BK>(base, kf, n_k, smem_base + buf_off, wave, nw, lane);
     }
   };
   // piece n of a block copy (full waves only), issued on its own
   auto stage_piece = [&](const __bf16* base, int kf, int buf_off, int n) {
-    const i32x4 rs = buffer_rsrc(base + (int64_t)kf * D, (uint32_t)(p.n_k - kf) * D * 2);
+    const i32x4 rs = buffer_rsrc(base + (int64_t)kf * D, (uint32_t)(n_k - kf) * D * 2);
     dma16_buf(dma_off[n], rs, smem_base + buf_off + wave * 1024 + n * NWF * 1024);
   };
   __syncthreads();  // the lists and the zeroed buffers are in LDS
 
   // Q^T fragments (B operands): query column 32 nq + l32, d = 16 ks + 8 hh + 0..7
-  const int64_t row_base = ((int64_t)b * p.h_q + hq) * p.n_q;
+  const int64_t row_base = sc.q0 + (int64_t)hq * sc.qh;
   bf16x8 qf[NQT][KS];
 #pragma unroll
   for (int nq = 0; nq < NQT; ++nq) {
     const int qp = q_first + nq * 32 + l32;
-    const bool ok = qp < p.n_q;
+    const bool ok = qp < n_q;
     const __bf16* qrow = q + (row_base + (ok ? qp : 0)) * D;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
@@ -520,7 +523,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   for (int nq = 0; nq < NQT; ++nq) {
     const float lt = l_run[nq] + __shfl_xor(l_run[nq], 32);
     const int qp = q_first + nq * 32 + l32;
-    if (qp >= p.n_q) continue;
+    if (qp >= n_q) continue;
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
     __bf16* orow = o + (row_base + qp) * D;
 #pragma unroll
@@ -545,8 +548,8 @@ hipError_t launch_waves(const cowa_params& p, const SchedView& sv, int hpw, int 
     const hipError_t err = allow_lds(reinterpret_cast<const void*>(kern), C::LDS_MAX);
     if (err != hipSuccess) return err;
   }
-  const unsigned blocks = (unsigned)sv.n_qt * n_hgroups * p.batch;
-  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * waves), C::lds_bytes(sv.n_kt), stream, p, sv, hpw,
+  const unsigned blocks = (unsigned)sv.n_qt * n_hgroups * (sv.ragged ? 1 : p.batch);
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * waves), C::lds_bytes(sv.max_kt), stream, p, sv, hpw,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), static_cast<const __bf16*>(v),
                      static_cast<__bf16*>(o), lse);
   return hipGetLastError();
@@ -556,7 +559,7 @@ template <int D, int BQ, int BK>
 hipError_t launch_cfg(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
                       void* o, float* lse, hipStream_t stream) {
   using C = FwdCfg<D, BQ, BK>;
-  if (sv.n_kt > C::max_kblocks()) return hipErrorInvalidValue;
+  if (sv.max_kt > C::max_kblocks()) return hipErrorInvalidValue;
   const int G = p.h_q / p.h_k;
   int hpw = 256 / BQ;  // QO heads per workgroup: up to 256 query rows
   while (hpw > 1 && G % hpw != 0) hpw >>= 1;

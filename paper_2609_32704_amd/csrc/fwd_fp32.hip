@@ -10,6 +10,7 @@
 // LSE = (m + log2 l) * ln 2 is the natural-log value the backward expects.
 #include "internal.h"
 #include "window_rule.h"
+#include "work_item.h"
 
 namespace cowa {
 namespace {
@@ -25,18 +26,22 @@ __global__ void __launch_bounds__(1024) fwd_fp32_kernel(cowa_params p, SchedView
   __shared__ float vs[kChunk][D];
 
   const int tq = p.tile_q, tk = p.tile_k;
-  const int i = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int hk = (int)(((int64_t)h * p.h_k) / p.h_q);
-  const HeadGeo g = make_geo(p.n_q, p.n_k, p.w_sink, p.w_near, tq, tk, p.h_k_offset + hk, p.h_k_total);
+  const int h = blockIdx.y;
+  const int hk_h = (int)(((int64_t)h * p.h_k) / p.h_q);
+  int hk;
+  const SeqCtx sc = seq_ctx(p, sv, blockIdx.x, sv.ragged ? hk_h : (int)blockIdx.z * p.h_k + hk_h, true, hk);
+  const int i = sc.tile;
+  const int n_q = sc.n_q, n_k = sc.n_k;
 
   const int tid = threadIdx.x;
   const int row = tid >> 3, sub = tid & 7;
   const int64_t qpos = (int64_t)i * tq + row;
-  const bool row_ok = qpos < p.n_q;
+  const bool row_ok = qpos < n_q;
+  const int64_t row_base = sc.q0 + (int64_t)h * sc.qh;
 
-  const float* qrow = q + (((int64_t)b * p.h_q + h) * p.n_q + (row_ok ? qpos : 0)) * D + sub * SL;
-  const float* kbase = k + ((int64_t)b * p.h_k + hk) * p.n_k * D;
-  const float* vbase = v + ((int64_t)b * p.h_k + hk) * p.n_k * D;
+  const float* qrow = q + (row_base + (row_ok ? qpos : 0)) * D + sub * SL;
+  const float* kbase = k + (sc.k0 + (int64_t)hk * sc.kh) * D;
+  const float* vbase = v + (sc.k0 + (int64_t)hk * sc.kh) * D;
 
   const float c = p.softmax_scale * 1.4426950408889634f;  // log2(e)
   float qr[SL], acc[SL];
@@ -44,7 +49,7 @@ __global__ void __launch_bounds__(1024) fwd_fp32_kernel(cowa_params p, SchedView
   for (int t = 0; t < SL; ++t) { qr[t] = row_ok ? qrow[t] : 0.f; acc[t] = 0.f; }
   float m = -INFINITY, l = 0.f;
 
-  const int r = hk * sv.n_qt + i;
+  const int r = sc.sched;
   const int e0 = sv.fwd_row_ptr[r], e1 = sv.fwd_row_ptr[r + 1];
   const int nthreads = blockDim.x;
   for (int e = e0; e < e1; ++e) {
@@ -57,7 +62,7 @@ __global__ void __launch_bounds__(1024) fwd_fp32_kernel(cowa_params p, SchedView
       for (int x = tid; x < kChunk * D; x += nthreads) {
         const int kk = x / D, dd = x % D;
         const int64_t kp = kfirst + kk;
-        const bool ok = kp < p.n_k;
+        const bool ok = kp < n_k;
         ks[kk][dd] = ok ? kbase[kp * D + dd] : 0.f;
         vs[kk][dd] = ok ? vbase[kp * D + dd] : 0.f;
       }
@@ -76,7 +81,7 @@ __global__ void __launch_bounds__(1024) fwd_fp32_kernel(cowa_params p, SchedView
           part += __shfl_xor(part, 4, 8);
           float sv2 = part * c;
           const int64_t kp = kfirst + kk;
-          if (kp >= p.n_k || (partial && !legal_pair(g, qpos, kp))) sv2 = -INFINITY;
+          if (kp >= n_k || (partial && !legal32(sc.g, (int)qpos, (int)kp))) sv2 = -INFINITY;
           s[u] = sv2;
           mx = fmaxf(mx, sv2);
         }
@@ -99,19 +104,19 @@ __global__ void __launch_bounds__(1024) fwd_fp32_kernel(cowa_params p, SchedView
     }
   }
   if (!row_ok) return;
-  float* orow = o + (((int64_t)b * p.h_q + h) * p.n_q + qpos) * D + sub * SL;
+  float* orow = o + (row_base + qpos) * D + sub * SL;
   const float inv = l > 0.f ? 1.f / l : 0.f;
 #pragma unroll
   for (int t = 0; t < SL; ++t) orow[t] = acc[t] * inv;
   if (sub == 0)
-    lse[((int64_t)b * p.h_q + h) * p.n_q + qpos] = l > 0.f ? (m + log2f(l)) * 0.6931471805599453f : -INFINITY;
+    lse[row_base + qpos] = l > 0.f ? (m + log2f(l)) * 0.6931471805599453f : -INFINITY;
 }
 
 }  // namespace
 
 hipError_t launch_fwd_fp32(const cowa_params& p, const SchedView& sv, const float* q, const float* k,
                            const float* v, float* o, float* lse, hipStream_t stream) {
-  dim3 grid(sv.n_qt, p.h_q, p.batch), block(p.tile_q * 8);
+  dim3 grid(sv.n_qt, p.h_q, sv.ragged ? 1 : p.batch), block(p.tile_q * 8);
   if (p.head_dim == 64)
     hipLaunchKernelGGL(fwd_fp32_kernel<64>, grid, block, 0, stream, p, sv, q, k, v, o, lse);
   else

@@ -8,25 +8,60 @@
 
 namespace cowa {
 
+// One sequence of a ragged batch (a table in the schedule buffer).
+struct SeqDesc {
+  int32_t q_start, k_start;  // first query / key position in the packed [H, N_total, d] tensors
+  int32_t n_q, n_k;          // its lengths
+  int32_t qt_off, kt_off;    // its first QO / KV block over the batch
+  int32_t pad0, pad1;
+};
+
+// Resolved window of one KV head (a table in the schedule buffer): sink and
+// near widths and the long-range distance bounds [lo, hi), clamped to 2^30
+// (a causal distance is always below N_k < 2^30).
+struct WinDesc {
+  int32_t sink, near, lo, hi;
+};
+
 // Device view of a built schedule.
 struct SchedView {
   const int32_t* fwd_row_ptr;
   const int32_t* bwd_col_ptr;
   const uint32_t* fwd_ent;
   const uint32_t* bwd_ent;
-  int32_t n_qt, n_kt;
+  const WinDesc* win;     // [n_win][h_k]: n_win = batch for a ragged batch under the default rule, else 1
+  const SeqDesc* seq;     // [batch], ragged batches only
+  const int32_t* qt_seq;  // [n_qt]: sequence of each QO block, ragged batches only
+  const int32_t* kt_seq;  // [n_kt]: sequence of each KV block, ragged batches only
+  int32_t n_qt, n_kt;     // QO / KV blocks: of one sequence (fixed lengths) or of the whole batch (ragged)
+  int32_t max_qt, max_kt; // QO / KV blocks of the longest sequence
+  int32_t ragged, per_seq_win;
 };
 
 inline SchedView sched_view(const cowa_schedule_t* s) {
   const char* b = static_cast<const char*>(s->buf);
+  const bool ragged = s->p.cu_seqlens_q != nullptr;
   SchedView v;
   v.fwd_row_ptr = reinterpret_cast<const int32_t*>(b + s->off_fwd_row_ptr);
   v.bwd_col_ptr = reinterpret_cast<const int32_t*>(b + s->off_bwd_col_ptr);
   v.fwd_ent = reinterpret_cast<const uint32_t*>(b + s->off_fwd_ent);
   v.bwd_ent = reinterpret_cast<const uint32_t*>(b + s->off_bwd_ent);
+  v.win = reinterpret_cast<const WinDesc*>(b + s->off_windows);
+  v.seq = ragged ? reinterpret_cast<const SeqDesc*>(b + s->off_seqs) : nullptr;
+  v.qt_seq = ragged ? reinterpret_cast<const int32_t*>(b + s->off_qt_seq) : nullptr;
+  v.kt_seq = ragged ? reinterpret_cast<const int32_t*>(b + s->off_kt_seq) : nullptr;
   v.n_qt = s->n_qt;
   v.n_kt = s->n_kt;
+  v.max_qt = s->max_qt;
+  v.max_kt = s->max_kt;
+  v.ragged = ragged ? 1 : 0;
+  v.per_seq_win = (ragged && s->p.windows == nullptr) ? 1 : 0;
   return v;
+}
+
+// Query rows (of d elements) in Q, O and dO: B H_q N_q, or H_q N_total when ragged.
+inline int64_t q_rows(const cowa_params& p) {
+  return (p.cu_seqlens_q ? 1 : (int64_t)p.batch) * p.h_q * p.n_q;
 }
 
 // Raise a kernel's dynamic LDS limit to `bytes`, once per (kernel, device);
@@ -34,7 +69,10 @@ inline SchedView sched_view(const cowa_schedule_t* s) {
 hipError_t allow_lds(const void* kernel, int bytes);
 
 // Each launcher enqueues on `stream` and returns hipGetLastError() of its launches.
-hipError_t launch_schedule(const cowa_schedule_t* s, hipStream_t stream);
+// Builds the schedule: uploads the host tables (windows, then the sequence
+// table of a ragged batch; `tables` holds their bytes laid out as in the
+// buffer from off_windows on), then counts, scans and fills the block lists.
+hipError_t launch_schedule(const cowa_schedule_t* s, const void* tables, size_t table_bytes, hipStream_t stream);
 
 hipError_t launch_fwd_fp32(const cowa_params& p, const SchedView& sv, const float* q, const float* k,
                            const float* v, float* o, float* lse, hipStream_t stream);
@@ -64,6 +102,9 @@ bool decode_supported(int head_dim, int group);
 size_t decode_workspace_bytes(const cowa_decode_params& p);
 int32_t decode_num_splits(const cowa_decode_params& p);
 int32_t decode_split_keys(const cowa_decode_params& p);
+
+// decode with explicit windows: at most this many local KV heads
+constexpr int kDecodeMaxExplicitHeads = 256;
 
 hipError_t launch_decode(const cowa_decode_params& p, const void* q, const void* k_cache,
                          const void* v_cache, const int32_t* seqlens, void* o, float* lse, void* ws,

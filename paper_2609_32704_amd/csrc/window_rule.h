@@ -37,6 +37,15 @@ __host__ __device__ inline void long_bounds(int64_t n_k, int64_t w_sink, int64_t
   *hi = w_near + ((hg + 1) * span) / ht;
 }
 
+// The same from resolved window bounds (sink, near, long-range [lo, hi)).
+__host__ __device__ inline HeadGeo make_geo_bounds(int32_t n_q, int32_t n_k, int32_t sink, int32_t near, int64_t lo,
+                                                   int64_t hi, int32_t tile_q, int32_t tile_k) {
+  HeadGeo g;
+  g.n_q = n_q; g.n_k = n_k; g.w_sink = sink; g.w_near = near; g.tile_q = tile_q; g.tile_k = tile_k;
+  g.lo = lo; g.hi = hi;
+  return g;
+}
+
 __host__ __device__ inline HeadGeo make_geo(int32_t n_q, int32_t n_k, int32_t w_sink, int32_t w_near,
                                             int32_t tile_q, int32_t tile_k, int32_t hg, int32_t ht) {
   HeadGeo g;

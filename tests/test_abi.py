@@ -45,11 +45,31 @@ def test_library_exports_every_declared_symbol():
     assert "gfx950" in abi.cowa_version()
 
 
-def test_struct_sizes_match_header_layout():
-    # int32 fields pack without padding; the schedule struct holds size_t offsets
-    assert ctypes.sizeof(abi.cowa_params) == 14 * 4
-    assert ctypes.sizeof(abi.cowa_decode_params) == 12 * 4
-    assert ctypes.sizeof(abi.cowa_window) == 16
+def test_struct_layouts_match_header(tmp_path):
+    """Every struct of the header has the same size and field offsets in C
+    (compiled here with gcc against include/cowa.h) as in the ctypes binding."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    structs = [abi.cowa_window, abi.cowa_params, abi.cowa_schedule_t, abi.cowa_decode_params]
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "cowa.h"', "int main(void) {"]
+    for st in structs:
+        lines.append(f'  printf("{st.__name__} %zu\\n", sizeof({st.__name__}));')
+        for name, _ in st._fields_:
+            lines.append(f'  printf("{st.__name__}.{name} %zu\\n", offsetof({st.__name__}, {name}));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = dict(line.split() for line in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                       check=True).stdout.splitlines())
+    for st in structs:
+        assert int(out[st.__name__]) == ctypes.sizeof(st), st.__name__
+        for name, _ in st._fields_:
+            assert int(out[f"{st.__name__}.{name}"]) == getattr(st, name).offset, f"{st.__name__}.{name}"
 
 
 @pytest.mark.parametrize("n_k,ws,wn,ht,ho,hk", [(131072, 128, 4096, 8, 0, 8), (512, 16, 64, 2, 0, 2),
@@ -252,3 +272,87 @@ def test_bwd_checks_every_stage_before_any_launch():
     # each stage on its own applies the same check
     st = lib.cowa_bwd_main(ctypes.byref(p), ctypes.byref(s), *[vp(1 << 24)] * 8, ctypes.c_size_t(need), vp(0))
     assert st == abi.COWA_ERR_UNSUPPORTED
+
+
+# ---- explicit window tuples and ragged batches (host side) ----
+
+RAGGED = [([0, 70, 70, 200, 233], [0, 100, 131, 300, 500]), ([0, 1], [0, 1]), ([0, 0, 5], [0, 3, 9]),
+          ([0, 300, 1000], [0, 300, 1000])]
+TUPLES = [None, [(1, 16, 5, 40), (0, 33, 0, 100), (50, 0, 3, 3)]]
+
+
+@pytest.mark.parametrize("cu", RAGGED)
+@pytest.mark.parametrize("tuples", TUPLES)
+def test_ragged_schedule_size_matches_oracle(cu, tuples):
+    cu_q, cu_k = cu
+    p = cowa.make_params(len(cu_q) - 1, cu_q[-1], cu_k[-1], 3, 3, 128, 4, 20, 64, 32, windows=tuples,
+                         cu_seqlens_q=cu_q, cu_seqlens_k=cu_k)
+    s = abi.cowa_schedule_size(p)
+    ref = osched.build_varlen(cu_q, cu_k, 64, 32, 4, 20, 3, windows=tuples)
+    assert s.nnz == len(ref["fwd_ent"])
+    assert (s.n_qt, s.n_kt) == (ref["n_qt"], ref["n_kt"])
+    rows, cols = np.diff(ref["fwd_row_ptr"]), np.diff(ref["bwd_col_ptr"])
+    assert s.max_row == (int(rows.max()) if rows.size else 0)
+    assert s.max_col == (int(cols.max()) if cols.size else 0)
+    lens_q, lens_k = np.diff(cu_q), np.diff(cu_k)
+    assert s.max_qt == int((-(-lens_q // 64)).max()) and s.max_kt == int((-(-lens_k // 32)).max())
+
+
+@pytest.mark.parametrize("tuples", TUPLES[1:])
+def test_tuple_schedule_size_matches_oracle(tuples):
+    p = cowa.make_params(2, 333, 1000, 6, 3, 128, 4, 20, 64, 128, windows=tuples)
+    s = abi.cowa_schedule_size(p)
+    ref = osched.build(333, 1000, 64, 128, 4, 20, 3, windows=tuples)
+    assert s.nnz == len(ref["fwd_ent"])
+    assert cowa.windows(p) == [tuple(t) for t in tuples]
+
+
+def test_legal_pairs_with_tuples_and_ragged():
+    from oracle import windows as w
+    cu_q, cu_k = [0, 70, 70, 200, 233], [0, 100, 131, 300, 500]
+    for tuples in TUPLES:
+        p = cowa.make_params(4, 233, 500, 6, 3, 128, 4, 20, 64, 32, windows=tuples, cu_seqlens_q=cu_q,
+                             cu_seqlens_k=cu_k)
+        ref = 0
+        for b in range(4):
+            n_q, n_k = cu_q[b + 1] - cu_q[b], cu_k[b + 1] - cu_k[b]
+            for h in range(3):
+                bounds = w.head_bounds(n_k, 4, 20, h, 3, None if tuples is None else tuples[h])
+                ref += int(w.visible_mask_bounds(n_q, n_k, *bounds).sum())
+        assert abi.cowa_legal_pairs(p) == 2 * ref
+
+
+@pytest.mark.parametrize("cu_q,cu_k", [([1, 5], [0, 5]), ([0, 6], [0, 5]), ([0, 5, 3], [0, 5, 9]),
+                                       ([0, 5], [0, 7])])
+def test_invalid_cu_seqlens_rejected(cu_q, cu_k):
+    lib = _lib()
+    p = cowa.make_params(len(cu_q) - 1, cu_q[-1], 5, 2, 1, 128, 1, 4, 64, 64, cu_seqlens_q=cu_q, cu_seqlens_k=cu_k)
+    s = abi.cowa_schedule_t()
+    assert lib.cowa_schedule_size(ctypes.byref(p), ctypes.byref(s)) == abi.COWA_ERR_INVALID_ARG
+
+
+def test_invalid_tuples_rejected():
+    lib = _lib()
+    p = cowa.make_params(1, 100, 100, 2, 2, 128, 1, 4, 64, 64, windows=[(1, 4, 0, 10), (1, -1, 0, 10)])
+    s = abi.cowa_schedule_t()
+    assert lib.cowa_schedule_size(ctypes.byref(p), ctypes.byref(s)) == abi.COWA_ERR_INVALID_ARG
+    d = cowa.make_decode_params(2, 4, 2, 128, 1000, 4, 8, windows=[(1, 4, 0, 10), (1, 4, -2, 10)])
+    n = ctypes.c_size_t()
+    assert lib.cowa_decode_workspace_size(ctypes.byref(d), ctypes.byref(n)) == abi.COWA_ERR_INVALID_ARG
+
+
+def test_schedule_digest_guards_windows_and_lengths():
+    """A schedule sized for one set of tuples or lengths is refused (before any
+    launch) for another of the same shapes."""
+    lib = _lib()
+    vp = ctypes.c_void_p
+    ok = 1 << 24
+    p1 = cowa.make_params(1, 256, 256, 4, 2, 128, 8, 32, 64, 64, windows=[(8, 32, 0, 50), (8, 32, 50, 50)])
+    s1 = _sized(p1)
+    p2 = cowa.make_params(1, 256, 256, 4, 2, 128, 8, 32, 64, 64, windows=[(8, 32, 0, 50), (8, 32, 51, 50)])
+    assert lib.cowa_fwd(ctypes.byref(p2), ctypes.byref(s1), *[vp(ok)] * 5, vp(0)) == abi.COWA_ERR_SCHEDULE_MISMATCH
+    r1 = cowa.make_params(2, 200, 300, 4, 2, 128, 8, 32, 64, 64, cu_seqlens_q=[0, 100, 200], cu_seqlens_k=[0, 150, 300])
+    sr = _sized(r1)
+    r2 = cowa.make_params(2, 200, 300, 4, 2, 128, 8, 32, 64, 64, cu_seqlens_q=[0, 90, 200], cu_seqlens_k=[0, 150, 300])
+    assert lib.cowa_fwd(ctypes.byref(r2), ctypes.byref(sr), *[vp(ok)] * 5, vp(0)) == abi.COWA_ERR_SCHEDULE_MISMATCH
+    assert lib.cowa_fwd(ctypes.byref(r1), ctypes.byref(sr), *[vp(ok)] * 5, vp(0)) == abi.COWA_ERR_NO_DEVICE

@@ -62,3 +62,39 @@ def test_schedule_random_shapes():
         hk = int(rng.integers(1, ht + 1))
         _check(n_q, n_k, int(rng.choice([32, 64, 128])), int(rng.choice([32, 64, 128])), int(rng.integers(0, 200)),
                int(rng.integers(0, 800)), hk, ht, int(rng.integers(0, ht - hk + 1)))
+
+
+def _check_general(p, ref):
+    import paper_2609_32704_amd as cowa
+    s = cowa.Schedule(p)
+    torch.cuda.synchronize()
+    got = {k: v.cpu().numpy() for k, v in s.arrays().items()}
+    assert s.nnz == len(ref["fwd_ent"])
+    for key in KEYS:
+        r = ref[key].astype(np.int64)
+        g = got[key].astype(np.int64) & 0xFFFFFFFF
+        assert np.array_equal(g, r), f"{key} differs"
+
+
+@pytest.mark.parametrize("cu_q,cu_k", [([0, 70, 70, 200, 233], [0, 100, 131, 300, 500]),
+                                       ([0, 1000, 1777, 2000], [0, 1000, 2000, 2500]),
+                                       ([0, 0, 0, 5], [0, 0, 3, 9])])
+@pytest.mark.parametrize("tuples", [None, [(1, 16, 5, 40), (0, 33, 0, 100), (50, 0, 3, 3)]])
+def test_schedule_ragged(cu_q, cu_k, tuples):
+    import paper_2609_32704_amd as cowa
+    need_gpu()
+    log(f"ragged schedule cu_q={cu_q} cu_k={cu_k} tuples={tuples}")
+    for tq, tk in ((64, 32), (128, 128)):
+        p = cowa.make_params(len(cu_q) - 1, cu_q[-1], cu_k[-1], 3, 3, 128, 4, 20, tq, tk, windows=tuples,
+                             cu_seqlens_q=cu_q, cu_seqlens_k=cu_k)
+        _check_general(p, oracle_schedule.build_varlen(cu_q, cu_k, tq, tk, 4, 20, 3, windows=tuples))
+
+
+@pytest.mark.parametrize("tuples", [[(1, 16, 5, 40), (0, 33, 0, 100), (50, 0, 3, 3)],
+                                    [(0, 1, 0, 10 ** 9), (7, 7, 10 ** 9, 10 ** 9), (2 ** 30, 0, 0, 0)]])
+def test_schedule_tuples(tuples):
+    import paper_2609_32704_amd as cowa
+    need_gpu()
+    for n_q, n_k, tq, tk in ((333, 1000, 64, 128), (1000, 1000, 128, 32)):
+        p = cowa.make_params(1, n_q, n_k, 3, 3, 128, 4, 20, tq, tk, windows=tuples)
+        _check_general(p, oracle_schedule.build(n_q, n_k, tq, tk, 4, 20, 3, windows=tuples))
