@@ -266,6 +266,21 @@ cowa_status cowa_decode(const cowa_decode_params* p, const void* q,
                         const int32_t* seqlens_k, void* o, float* lse,
                         void* workspace, size_t ws_bytes, void* stream);
 
+/* cowa_decode without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation): the same kernels and results as cowa_decode, with the
+ * split partials in a device array inside the library (32 MiB per GPU, held
+ * until the process ends; looked up once per device).  Allocates nothing.
+ * Returns COWA_ERR_UNSUPPORTED (before any launch) when cowa_decode_workspace_size
+ * of `p` exceeds 32 MiB (e.g. 64 sequences x 32 QO heads x d = 128 use 2 MiB at
+ * the default split size).  Every call on one GPU shares that GPU's array:
+ * calls that overlap on one GPU (different streams or host threads) race and
+ * must be serialised by the caller.  Nothing in the array needs clearing: each
+ * call overwrites every partial it reads. */
+cowa_status cowa_decode_noalloc(const cowa_decode_params* p, const void* q,
+                                const void* k_cache, const void* v_cache,
+                                const int32_t* seqlens_k, void* o, float* lse, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

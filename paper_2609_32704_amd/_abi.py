@@ -95,6 +95,7 @@ _SIGNATURES = {
     "cowa_decode_workspace_size": (ctypes.c_int, [_P(cowa_decode_params), _P(ctypes.c_size_t)]),
     "cowa_decode": (ctypes.c_int, [_P(cowa_decode_params), _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t,
                                    _vp]),
+    "cowa_decode_noalloc": (ctypes.c_int, [_P(cowa_decode_params), _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
 }
 
 _lib = None
@@ -205,3 +206,8 @@ def cowa_decode_workspace_size(dparams):
 def cowa_decode(dparams, q, k_cache, v_cache, seqlens_k, o, lse, workspace, ws_bytes, stream):
     check(lib().cowa_decode(ctypes.byref(dparams), _vp(q), _vp(k_cache), _vp(v_cache), _vp(seqlens_k), _vp(o),
                             _vp(lse), _vp(workspace), ws_bytes, _vp(stream)))
+
+
+def cowa_decode_noalloc(dparams, q, k_cache, v_cache, seqlens_k, o, lse, stream):
+    check(lib().cowa_decode_noalloc(ctypes.byref(dparams), _vp(q), _vp(k_cache), _vp(v_cache), _vp(seqlens_k),
+                                    _vp(o), _vp(lse), _vp(stream)))

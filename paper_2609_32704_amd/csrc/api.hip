@@ -637,4 +637,28 @@ cowa_status cowa_decode(const cowa_decode_params* p, const void* q, const void* 
                     "decode launch");
 }
 
+cowa_status cowa_decode_noalloc(const cowa_decode_params* p, const void* q, const void* k_cache, const void* v_cache,
+                                const int32_t* seqlens_k, void* o, float* lse, void* stream) {
+  COWA_TRY(check_decode_params(p));
+  if (p->batch == 0) return COWA_OK;
+  COWA_TRY(check_tensor(q, "q", 16));
+  COWA_TRY(check_tensor(k_cache, "k_cache", 16));
+  COWA_TRY(check_tensor(v_cache, "v_cache", 16));
+  COWA_TRY(check_tensor(seqlens_k, "seqlens_k", 4));
+  COWA_TRY(check_tensor(o, "o", 16));
+  COWA_TRY(check_tensor(lse, "lse", 4));
+  const size_t need = cowa::decode_workspace_bytes(*p);
+  if (need > cowa::kDecodeScratchBytes)
+    return fail(COWA_ERR_UNSUPPORTED,
+                "cowa_decode_noalloc: this step needs %zu bytes of split partials, more than its %zu-byte device "
+                "scratch; use cowa_decode with a workspace, or a larger split_keys",
+                need, cowa::kDecodeScratchBytes);
+  COWA_TRY(check_device());
+  void* ws = nullptr;
+  COWA_TRY(hip_status(cowa::decode_scratch(&ws), "decode scratch address"));
+  return hip_status(cowa::launch_decode(*p, q, k_cache, v_cache, seqlens_k, o, lse, ws,
+                                        static_cast<hipStream_t>(stream)),
+                    "decode launch");
+}
+
 }  // extern "C"

@@ -13,6 +13,9 @@
 // Combine kernel: one 64-lane wave per (sequence, QO head) merges the split
 // partials (max of m, rescaled sums) and writes O and the natural-log LSE.
 // Everything is fp32 apart from the bf16 loads; scores are kept in base 2.
+#include <map>
+#include <mutex>
+
 #include "internal.h"
 #include "window_rule.h"
 
@@ -376,6 +379,32 @@ size_t decode_workspace_bytes(const cowa_decode_params& p) {
   const size_t parts = (size_t)p.batch * p.h_q * decode_num_splits(p);
   const size_t o_bytes = (parts * p.head_dim * sizeof(float) + 255) & ~size_t(255);
   return o_bytes + ((parts * 2 * sizeof(float) + 255) & ~size_t(255));
+}
+
+// Scratch of the allocation-free decoding entry point: the split partials live
+// in this file-scope device array (one copy per GPU, held until the process
+// ends) instead of a caller workspace.  Host code never uses the array's name
+// as an address: decode_scratch() looks the device address up once per device
+// and every launch takes that pointer.
+__device__ __align__(256) unsigned char scratch[kDecodeScratchBytes];
+
+hipError_t decode_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) return err;
+  static std::mutex mu;
+  static std::map<int, void*> addr;  // device -> address of its copy of `scratch`
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = addr.find(dev);
+  if (it == addr.end()) {
+    void* a = nullptr;
+    err = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch));
+    if (err != hipSuccess) return err;
+    if (a == nullptr) return hipErrorInvalidSymbol;
+    it = addr.emplace(dev, a).first;
+  }
+  *ptr = it->second;
+  return hipSuccess;
 }
 
 bool decode_supported(int head_dim, int group) {

@@ -106,6 +106,12 @@ int32_t decode_split_keys(const cowa_decode_params& p);
 // decode with explicit windows: at most this many local KV heads
 constexpr int kDecodeMaxExplicitHeads = 256;
 
+// The allocation-free decoding entry point keeps its split partials in a
+// device array of this many bytes (per GPU); decode_scratch() gives the
+// current device's address of it (looked up once per device).
+constexpr size_t kDecodeScratchBytes = size_t(32) << 20;
+hipError_t decode_scratch(void** ptr);
+
 hipError_t launch_decode(const cowa_decode_params& p, const void* q, const void* k_cache,
                          const void* v_cache, const int32_t* seqlens, void* o, float* lse, void* ws,
                          hipStream_t stream);

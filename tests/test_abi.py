@@ -356,3 +356,18 @@ def test_schedule_digest_guards_windows_and_lengths():
     r2 = cowa.make_params(2, 200, 300, 4, 2, 128, 8, 32, 64, 64, cu_seqlens_q=[0, 90, 200], cu_seqlens_k=[0, 150, 300])
     assert lib.cowa_fwd(ctypes.byref(r2), ctypes.byref(sr), *[vp(ok)] * 5, vp(0)) == abi.COWA_ERR_SCHEDULE_MISMATCH
     assert lib.cowa_fwd(ctypes.byref(r1), ctypes.byref(sr), *[vp(ok)] * 5, vp(0)) == abi.COWA_ERR_NO_DEVICE
+
+
+def test_decode_noalloc_rejects_steps_beyond_its_scratch():
+    """The allocation-free decode keeps split partials in a 32 MiB device
+    array; a step that needs more is refused before any device call."""
+    lib = _lib()
+    vp = ctypes.c_void_p
+    ok = 1 << 24
+    big = cowa.make_decode_params(256, 64, 8, 128, 131072, 128, 4096, split_keys=64)
+    assert abi.cowa_decode_workspace_size(big) > 32 << 20
+    assert lib.cowa_decode_noalloc(ctypes.byref(big), *[vp(ok)] * 6, vp(0)) == abi.COWA_ERR_UNSUPPORTED
+    assert b"scratch" in lib.cowa_last_error()
+    fits = cowa.make_decode_params(64, 32, 8, 128, 131072, 128, 4096)
+    assert abi.cowa_decode_workspace_size(fits) <= 32 << 20
+    assert lib.cowa_decode_noalloc(ctypes.byref(fits), *[vp(ok)] * 6, vp(0)) == abi.COWA_ERR_NO_DEVICE
