@@ -19,11 +19,16 @@ generator seeded with 42, resident in HBM before timing starts.
 Extra blocks in the JSON line:
   roofline      the dominant kernel (backward main pass) against the bf16
                 MFMA peak; traffic from committed rocprofv3 counter summaries
-  kernels       every kernel's time, work and roofline fraction
+  kernels       every kernel's time, work and roofline fraction (decode with
+                its counter bytes over the algorithmic bytes)
+  workloads     forward / backward times and fractions at 8192 tokens and at
+                2 x 32768 tokens, and one rank's share of the 131072-token
+                step in the paper's 8-way KV-head tensor parallelism (1 KV
+                head, 4 QO heads, global KV head 0 = heaviest and 7 = lightest)
   dense         the same kernels in dense causal mode (w_sink = 0,
                 w_near = N), the in-house FullAttn twin, and CoWA/dense ratios
   cpu_baseline  the fp64 CPU oracle timed on a bounded sample of the same
-                workload on this host
+                workload on this host (with the host's CPU model and memory)
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
@@ -77,6 +82,23 @@ def read_traffic(kernel):
     return None
 
 
+def host_info():
+    """CPU model, logical CPUs and memory of this host."""
+    model, mem_gb = "unknown", None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+        for line in open("/proc/meminfo"):
+            if line.startswith("MemTotal"):
+                mem_gb = round(int(line.split()[1]) / 1024 ** 2, 1)
+                break
+    except OSError:
+        pass
+    return {"cpu_model": model, "logical_cpus": os.cpu_count(), "ram_gib": mem_gb}
+
+
 def cpu_baseline(target_s=12.0):
     """The fp64 oracle (as it stands) on a bounded sample of the 128K training
     workload: every QO-head row of a few 128-row query blocks, full forward
@@ -109,7 +131,7 @@ def cpu_baseline(target_s=12.0):
         blocks.append((h, blk))
     flops = 14 * w.head_dim * done_pairs
     return {"value": flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "seconds": round(elapsed, 3),
+            "seconds": round(elapsed, 3), "host": host_info(),
             "sample": f"{len(blocks)} (QO head, 128-row query block) pairs of the 131072-token workload, "
                       f"full fp64 forward+backward of those rows ({done_pairs} legal pairs, 14d FLOPs each)"}
 
@@ -122,6 +144,7 @@ def main():
     ap.add_argument("--dense-iters", type=int, default=2)
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-workloads", action="store_true", help="skip the 8K / 32K / per-rank timings")
     ap.add_argument("--only", choices=["all", "train", "decode", "copy"], default="all",
                     help="profiling aid: run only part of the step (the JSON line is printed for 'all' only)")
     args = ap.parse_args()
@@ -213,13 +236,13 @@ def main():
         evs[1].record()
         _abi.cowa_fwd(p, sched.s, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), stream)
         evs[2].record()
-        _abi.cowa_bwd_prepare(p, o.data_ptr(), do.data_ptr(), ws.data_ptr(), ws_bytes, stream)
+        _abi.cowa_bwd_prepare(p, o.data_ptr(), do.data_ptr(), lse.data_ptr(), ws.data_ptr(), ws_bytes, stream)
         evs[3].record()
-        _abi.cowa_bwd_main(p, sched.s, q.data_ptr(), k.data_ptr(), v.data_ptr(), lse.data_ptr(), do.data_ptr(),
-                           dk.data_ptr(), dv.data_ptr(), ws.data_ptr(), ws_bytes, stream)
+        _abi.cowa_bwd_main(p, sched.s, q.data_ptr(), k.data_ptr(), v.data_ptr(), do.data_ptr(), dk.data_ptr(),
+                           dv.data_ptr(), ws.data_ptr(), ws_bytes, stream)
         evs[4].record()
-        _abi.cowa_bwd_dq(p, sched.s, q.data_ptr(), k.data_ptr(), v.data_ptr(), lse.data_ptr(), do.data_ptr(),
-                         dq.data_ptr(), ws.data_ptr(), ws_bytes, stream)
+        _abi.cowa_bwd_dq(p, sched.s, q.data_ptr(), k.data_ptr(), v.data_ptr(), do.data_ptr(), dq.data_ptr(),
+                         ws.data_ptr(), ws_bytes, stream)
         evs[5].record()
         if do_decode:
             _abi.cowa_decode(dpar, dq_in.data_ptr(), kc.data_ptr(), vc.data_ptr(), seqlens.data_ptr(),
@@ -259,8 +282,9 @@ def main():
         "schedule": {"ms": per["schedule"], "bound": "launch", "note": "three small kernels"},
         "fwd": {"ms": per["fwd"], "bound": "mfma", "work": fwd_flops, "unit": "TFLOP/s",
                 "achieved": fwd_flops / (per["fwd"] * 1e-3) / 1e12},
-        "bwd_prepare": {"ms": per["bwd_prepare"], "bound": "hbm", "unit": "GB/s", "work": 2 * elem_q * 2 + rows_q * 4,
-                        "achieved": (2 * elem_q * 2 + rows_q * 4) / (per["bwd_prepare"] * 1e-3) / 1e9},
+        # reads O, dO and LSE, writes -D and -LSE log2(e)
+        "bwd_prepare": {"ms": per["bwd_prepare"], "bound": "hbm", "unit": "GB/s", "work": 2 * elem_q * 2 + rows_q * 12,
+                        "achieved": (2 * elem_q * 2 + rows_q * 12) / (per["bwd_prepare"] * 1e-3) / 1e9},
         # algorithmic share of the backward's 10d per pair: the dK/dV pass does the
         # recompute of S and dP plus dV and dK (8d); the dQ pass adds dQ (2d) and
         # recomputes S and dP again (4d executed on top, not counted)
@@ -284,6 +308,67 @@ def main():
                 "achieved": main_k["achieved"], "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": main_k["frac"], "traffic": traffic,
                 "work_per_launch": f"{8 * T['d'] * pairs:.4e} FLOP = 8 d x {pairs} legal pairs"}
+
+    # decode: counter bytes (both kernels) over the algorithmic bytes
+    t_split, t_comb = read_traffic("decode_split"), read_traffic("decode_combine")
+    if t_split is not None and t_comb is not None:
+        kernels["decode"]["traffic"] = t_split + t_comb
+        kernels["decode"]["traffic_over_algorithmic"] = (t_split + t_comb) / dec_bytes
+
+    workloads = None
+    if not args.no_workloads:
+        log("other workloads: 8192 tokens, 2 x 32768 tokens, per-rank shares of the 131072-token step")
+        workloads = {}
+
+        def time_train(par, tq, tk, tv, tdo, iters):
+            """Mean ms of schedule+forward and of the backward, HIP events on the launch stream."""
+            sch = cowa.Schedule(par, dev, build=False)
+            o_ = torch.empty_like(tq)
+            lse_ = torch.empty(tq.shape[:3], dtype=torch.float32, device=dev)
+            dq_, dk_, dv_ = torch.empty_like(tq), torch.empty_like(tk), torch.empty_like(tv)
+            wsb = _abi.cowa_bwd_workspace_size(par)
+            ws_ = torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
+            tf = tb = 0.0
+            for it in range(iters + 1):
+                e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+                e[0].record()
+                _abi.cowa_schedule(sch.s, stream)
+                _abi.cowa_fwd(par, sch.s, tq.data_ptr(), tk.data_ptr(), tv.data_ptr(), o_.data_ptr(),
+                              lse_.data_ptr(), stream)
+                e[1].record()
+                _abi.cowa_bwd(par, sch.s, tq.data_ptr(), tk.data_ptr(), tv.data_ptr(), o_.data_ptr(), lse_.data_ptr(),
+                              tdo.data_ptr(), dq_.data_ptr(), dk_.data_ptr(), dv_.data_ptr(), ws_.data_ptr(), wsb,
+                              stream)
+                e[2].record()
+                torch.cuda.synchronize()
+                if it:
+                    tf += e[0].elapsed_time(e[1]) / iters
+                    tb += e[1].elapsed_time(e[2]) / iters
+            pr = _abi.cowa_legal_pairs(par)
+            d_ = par.head_dim
+            return {"fwd_ms": tf, "bwd_ms": tb, "legal_pairs": pr,
+                    "fwd_tflops": 4 * d_ * pr / (tf * 1e-3) / 1e12, "bwd_tflops": 10 * d_ * pr / (tb * 1e-3) / 1e12,
+                    "fwd_frac": 4 * d_ * pr / (tf * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                    "bwd_frac": 10 * d_ * pr / (tb * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
+
+        for name, (bsz, n, ws_w, wn_w, tile) in (("bf16_t8k", (1, 8192, 64, 1024, 64)),
+                                                ("bf16_t32k_b2", (2, 32768, 64, 2048, 128))):
+            tq2, tk2 = randn((bsz, 32, n, 128)), randn((bsz, 8, n, 128))
+            tv2, tdo2 = randn((bsz, 8, n, 128)), randn((bsz, 32, n, 128))
+            par = cowa.make_params(bsz, n, n, 32, 8, 128, ws_w, wn_w, tile, tile)
+            workloads[name] = dict(time_train(par, tq2, tk2, tv2, tdo2, 10),
+                                   shape=f"B={bsz}, T={n}, 32 QO / 8 KV heads, d=128, sink {ws_w}, near {wn_w}, "
+                                         f"{tile}x{tile} blocks")
+            del tq2, tk2, tv2, tdo2
+        if do_train:
+            # one rank of the 8-way KV-head split: its KV head (global index r) and the 4 QO heads
+            # of that head's group (contiguous leading heads of the 131072-token tensors)
+            for r in (0, 7):
+                par = cowa.make_params(1, T["n"], T["n"], 4, 1, T["d"], T["w_sink"], T["w_near"], T["tile"],
+                                       T["tile"], h_k_total=8, h_k_offset=r)
+                workloads[f"tp8_rank{r}"] = dict(
+                    time_train(par, q[:, :4], k[:, :1], v[:, :1], do[:, :4], 5),
+                    shape=f"131072 tokens, one rank of 8: global KV head {r}, 4 QO heads")
 
     dense = None
     if not args.no_dense and args.dense_iters > 0:
@@ -341,7 +426,7 @@ def main():
         "bwd_tflops": bwd_flops / (bwd_ms * 1e-3) / 1e12,
         "decode_ms": per["decode"], "decode_gbps": dec_bytes / (per["decode"] * 1e-3) / 1e9,
         "legal_pairs": pairs, "decode_visible_keys": vis_keys,
-        "roofline": roofline, "kernels": kernels, "dense": dense, "cpu_baseline": cpu,
+        "roofline": roofline, "kernels": kernels, "workloads": workloads, "dense": dense, "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
 

@@ -202,8 +202,9 @@ cowa_status cowa_fwd(const cowa_params* p, const cowa_schedule_t* s,
                      const void* q, const void* k, const void* v,
                      void* o, float* lse, void* stream);
 
-/* Workspace bytes cowa_bwd needs: the float32 row sums D = rowsum(O * dO)
- * of Alg. 2, one per query row. */
+/* Workspace bytes cowa_bwd needs: per query row, the float32 -D with
+ * D = rowsum(O * dO) (the term of Alg. 2) and -LSE log2(e) (the row's
+ * exponent offset in base 2): two arrays in the row layout of LSE. */
 cowa_status cowa_bwd_workspace_size(const cowa_params* p, size_t* bytes);
 
 /* Backward (Alg. 2): exact gradients of <dO, O> w.r.t. the unscaled Q, K and
@@ -223,9 +224,10 @@ cowa_status cowa_bwd(const cowa_params* p, const cowa_schedule_t* s,
                      void* dq, void* dk, void* dv,
                      void* workspace, size_t ws_bytes, void* stream);
 
-/* Backward stage 1: D = rowsum(O * dO) (the term subtracted from dP in
- * Alg. 2) into the workspace. */
-cowa_status cowa_bwd_prepare(const cowa_params* p, const void* o, const void* d_o,
+/* Backward stage 1: the per-row values of Alg. 2 into the workspace -- -D with
+ * D = rowsum(O * dO) (subtracted from dP), and -LSE log2(e) from the saved
+ * natural-log LSE of the forward (the offset that rebuilds P = exp(S - LSE)). */
+cowa_status cowa_bwd_prepare(const cowa_params* p, const void* o, const void* d_o, const float* lse,
                              void* workspace, size_t ws_bytes, void* stream);
 
 /* Backward stage 2, dK and dV (the loop of Alg. 2 over QO blocks): for every
@@ -235,7 +237,7 @@ cowa_status cowa_bwd_prepare(const cowa_params* p, const void* o, const void* d_
  * the workspace filled by cowa_bwd_prepare. */
 cowa_status cowa_bwd_main(const cowa_params* p, const cowa_schedule_t* s,
                           const void* q, const void* k, const void* v,
-                          const float* lse, const void* d_o, void* dk, void* dv,
+                          const void* d_o, void* dk, void* dv,
                           void* workspace, size_t ws_bytes, void* stream);
 
 /* Backward stage 3, dQ: for every QO head and QO block, over the KV blocks of
@@ -244,7 +246,7 @@ cowa_status cowa_bwd_main(const cowa_params* p, const cowa_schedule_t* s,
  * pass avoids them.)  Needs the workspace filled by cowa_bwd_prepare. */
 cowa_status cowa_bwd_dq(const cowa_params* p, const cowa_schedule_t* s,
                         const void* q, const void* k, const void* v,
-                        const float* lse, const void* d_o, void* dq,
+                        const void* d_o, void* dq,
                         void* workspace, size_t ws_bytes, void* stream);
 
 /* Workspace bytes of one decoding step (Sec. 2.3, decoding execution): the

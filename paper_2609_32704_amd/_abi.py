@@ -87,10 +87,10 @@ _SIGNATURES = {
     "cowa_bwd_workspace_size": (ctypes.c_int, [_P(cowa_params), _P(ctypes.c_size_t)]),
     "cowa_bwd": (ctypes.c_int, [_P(cowa_params), _P(cowa_schedule_t), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                 _vp, _vp, ctypes.c_size_t, _vp]),
-    "cowa_bwd_prepare": (ctypes.c_int, [_P(cowa_params), _vp, _vp, _vp, ctypes.c_size_t, _vp]),
-    "cowa_bwd_main": (ctypes.c_int, [_P(cowa_params), _P(cowa_schedule_t), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+    "cowa_bwd_prepare": (ctypes.c_int, [_P(cowa_params), _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+    "cowa_bwd_main": (ctypes.c_int, [_P(cowa_params), _P(cowa_schedule_t), _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                      ctypes.c_size_t, _vp]),
-    "cowa_bwd_dq": (ctypes.c_int, [_P(cowa_params), _P(cowa_schedule_t), _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+    "cowa_bwd_dq": (ctypes.c_int, [_P(cowa_params), _P(cowa_schedule_t), _vp, _vp, _vp, _vp, _vp, _vp,
                                    ctypes.c_size_t, _vp]),
     "cowa_decode_workspace_size": (ctypes.c_int, [_P(cowa_decode_params), _P(ctypes.c_size_t)]),
     "cowa_decode": (ctypes.c_int, [_P(cowa_decode_params), _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t,
@@ -183,18 +183,19 @@ def cowa_bwd(params, sched, q, k, v, o, lse, d_o, dq, dk, dv, workspace, ws_byte
                          _vp(d_o), _vp(dq), _vp(dk), _vp(dv), _vp(workspace), ws_bytes, _vp(stream)))
 
 
-def cowa_bwd_prepare(params, o, d_o, workspace, ws_bytes, stream):
-    check(lib().cowa_bwd_prepare(ctypes.byref(params), _vp(o), _vp(d_o), _vp(workspace), ws_bytes, _vp(stream)))
+def cowa_bwd_prepare(params, o, d_o, lse, workspace, ws_bytes, stream):
+    check(lib().cowa_bwd_prepare(ctypes.byref(params), _vp(o), _vp(d_o), _vp(lse), _vp(workspace), ws_bytes,
+                                 _vp(stream)))
 
 
-def cowa_bwd_main(params, sched, q, k, v, lse, d_o, dk, dv, workspace, ws_bytes, stream):
-    check(lib().cowa_bwd_main(ctypes.byref(params), ctypes.byref(sched), _vp(q), _vp(k), _vp(v), _vp(lse),
-                              _vp(d_o), _vp(dk), _vp(dv), _vp(workspace), ws_bytes, _vp(stream)))
+def cowa_bwd_main(params, sched, q, k, v, d_o, dk, dv, workspace, ws_bytes, stream):
+    check(lib().cowa_bwd_main(ctypes.byref(params), ctypes.byref(sched), _vp(q), _vp(k), _vp(v), _vp(d_o),
+                              _vp(dk), _vp(dv), _vp(workspace), ws_bytes, _vp(stream)))
 
 
-def cowa_bwd_dq(params, sched, q, k, v, lse, d_o, dq, workspace, ws_bytes, stream):
-    check(lib().cowa_bwd_dq(ctypes.byref(params), ctypes.byref(sched), _vp(q), _vp(k), _vp(v), _vp(lse), _vp(d_o),
-                            _vp(dq), _vp(workspace), ws_bytes, _vp(stream)))
+def cowa_bwd_dq(params, sched, q, k, v, d_o, dq, workspace, ws_bytes, stream):
+    check(lib().cowa_bwd_dq(ctypes.byref(params), ctypes.byref(sched), _vp(q), _vp(k), _vp(v), _vp(d_o), _vp(dq),
+                            _vp(workspace), ws_bytes, _vp(stream)))
 
 
 def cowa_decode_workspace_size(dparams):

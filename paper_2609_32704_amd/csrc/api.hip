@@ -476,12 +476,13 @@ cowa_status cowa_fwd(const cowa_params* p, const cowa_schedule_t* s, const void*
 cowa_status cowa_bwd_workspace_size(const cowa_params* p, size_t* bytes) {
   COWA_TRY(check_params(p));
   if (!bytes) return fail(COWA_ERR_INVALID_ARG, "bytes is NULL");
-  *bytes = align256((size_t)cowa::q_rows(*p) * sizeof(float));
+  *bytes = 2 * cowa::bwd_array_bytes(*p);
   return COWA_OK;
 }
 
-// Checks shared by the backward stages; the workspace holds D = rowsum(O * dO).
-static cowa_status check_bwd(const cowa_params* p, const Layout& L, size_t ws_bytes, void* workspace, float** dsum) {
+// Checks shared by the backward stages; the workspace holds -D and -LSE log2(e) per query row.
+static cowa_status check_bwd(const cowa_params* p, const Layout& L, size_t ws_bytes, void* workspace,
+                             cowa::BwdWork* w) {
   if (p->dtype != COWA_BF16) return fail(COWA_ERR_UNSUPPORTED, "backward is built for bf16 only");
   if (!cowa::bwd_bf16_supported(p->head_dim, p->tile_q, p->tile_k))
     return fail(COWA_ERR_UNSUPPORTED, "bf16 backward is built for tile_q, tile_k in {64, 128} (got %d x %d)",
@@ -503,84 +504,82 @@ static cowa_status check_bwd(const cowa_params* p, const Layout& L, size_t ws_by
   COWA_TRY(cowa_bwd_workspace_size(p, &need));
   if (!no_work(p) && (!workspace || ws_bytes < need || !aligned(workspace, 256)))
     return fail(COWA_ERR_WORKSPACE, "backward needs a 256-byte aligned workspace of %zu bytes (got %zu)", need, ws_bytes);
-  *dsum = static_cast<float*>(workspace);
+  *w = cowa::bwd_work(*p, workspace);
   return COWA_OK;
 }
 
 // Pointer checks of each stage (after check_bwd, when there is work).
-static cowa_status check_prepare_ptrs(const void* o, const void* d_o) {
+static cowa_status check_prepare_ptrs(const void* o, const void* d_o, const float* lse) {
   COWA_TRY(check_tensor(o, "o", 16));
-  return check_tensor(d_o, "d_o", 16);
-}
-
-static cowa_status check_qkv_lse_do(const void* q, const void* k, const void* v, const float* lse, const void* d_o) {
-  COWA_TRY(check_tensor(q, "q", 16));
-  COWA_TRY(check_tensor(k, "k", 16));
-  COWA_TRY(check_tensor(v, "v", 16));
   COWA_TRY(check_tensor(lse, "lse", 4));
   return check_tensor(d_o, "d_o", 16);
 }
 
-static cowa_status check_main_ptrs(const void* q, const void* k, const void* v, const float* lse, const void* d_o,
-                                   const void* dk, const void* dv) {
-  COWA_TRY(check_qkv_lse_do(q, k, v, lse, d_o));
+static cowa_status check_qkv_do(const void* q, const void* k, const void* v, const void* d_o) {
+  COWA_TRY(check_tensor(q, "q", 16));
+  COWA_TRY(check_tensor(k, "k", 16));
+  COWA_TRY(check_tensor(v, "v", 16));
+  return check_tensor(d_o, "d_o", 16);
+}
+
+static cowa_status check_main_ptrs(const void* q, const void* k, const void* v, const void* d_o, const void* dk,
+                                   const void* dv) {
+  COWA_TRY(check_qkv_do(q, k, v, d_o));
   COWA_TRY(check_tensor(dk, "dk", 16));
   return check_tensor(dv, "dv", 16);
 }
 
-static cowa_status check_dq_ptrs(const void* q, const void* k, const void* v, const float* lse, const void* d_o,
-                                 const void* dq) {
-  COWA_TRY(check_qkv_lse_do(q, k, v, lse, d_o));
+static cowa_status check_dq_ptrs(const void* q, const void* k, const void* v, const void* d_o, const void* dq) {
+  COWA_TRY(check_qkv_do(q, k, v, d_o));
   return check_tensor(dq, "dq", 16);
 }
 
-cowa_status cowa_bwd_prepare(const cowa_params* p, const void* o, const void* d_o, void* workspace, size_t ws_bytes,
-                             void* stream) {
+cowa_status cowa_bwd_prepare(const cowa_params* p, const void* o, const void* d_o, const float* lse, void* workspace,
+                             size_t ws_bytes, void* stream) {
   COWA_TRY(check_params(p));
   Layout L;
   COWA_TRY(resolve_layout(p, &L));
-  float* dsum;
-  COWA_TRY(check_bwd(p, L, ws_bytes, workspace, &dsum));
+  cowa::BwdWork w;
+  COWA_TRY(check_bwd(p, L, ws_bytes, workspace, &w));
   if (no_work(p)) return COWA_OK;
-  COWA_TRY(check_prepare_ptrs(o, d_o));
+  COWA_TRY(check_prepare_ptrs(o, d_o, lse));
   COWA_TRY(check_device());
   if (cowa::q_rows(*p) == 0) return COWA_OK;
-  return hip_status(cowa::launch_bwd_prepare(*p, o, d_o, dsum, static_cast<hipStream_t>(stream)),
+  return hip_status(cowa::launch_bwd_prepare(*p, o, d_o, lse, w, static_cast<hipStream_t>(stream)),
                     "backward prepare launch");
 }
 
 cowa_status cowa_bwd_main(const cowa_params* p, const cowa_schedule_t* s, const void* q, const void* k,
-                          const void* v, const float* lse, const void* d_o, void* dk, void* dv, void* workspace,
-                          size_t ws_bytes, void* stream) {
+                          const void* v, const void* d_o, void* dk, void* dv, void* workspace, size_t ws_bytes,
+                          void* stream) {
   COWA_TRY(check_params(p));
   Layout L;
   COWA_TRY(resolve_layout(p, &L));
-  float* dsum;
-  COWA_TRY(check_bwd(p, L, ws_bytes, workspace, &dsum));
+  cowa::BwdWork w;
+  COWA_TRY(check_bwd(p, L, ws_bytes, workspace, &w));
   COWA_TRY(check_schedule(p, L, s));
   if (no_work(p)) return COWA_OK;
-  COWA_TRY(check_main_ptrs(q, k, v, lse, d_o, dk, dv));
+  COWA_TRY(check_main_ptrs(q, k, v, d_o, dk, dv));
   COWA_TRY(check_device());
   if (s->n_kt == 0) return COWA_OK;
-  return hip_status(cowa::launch_bwd_main(*p, cowa::sched_view(s), q, k, v, lse, d_o, dk, dv, dsum,
+  return hip_status(cowa::launch_bwd_main(*p, cowa::sched_view(s), q, k, v, d_o, dk, dv, w,
                                           static_cast<hipStream_t>(stream)),
                     "backward dK/dV launch");
 }
 
 cowa_status cowa_bwd_dq(const cowa_params* p, const cowa_schedule_t* s, const void* q, const void* k, const void* v,
-                        const float* lse, const void* d_o, void* dq, void* workspace, size_t ws_bytes,
-                        void* stream) {
+                        const void* d_o, void* dq, void* workspace, size_t ws_bytes, void* stream) {
   COWA_TRY(check_params(p));
   Layout L;
   COWA_TRY(resolve_layout(p, &L));
-  float* dsum;
-  COWA_TRY(check_bwd(p, L, ws_bytes, workspace, &dsum));
+  cowa::BwdWork w;
+  COWA_TRY(check_bwd(p, L, ws_bytes, workspace, &w));
   COWA_TRY(check_schedule(p, L, s));
   if (no_work(p)) return COWA_OK;
-  COWA_TRY(check_dq_ptrs(q, k, v, lse, d_o, dq));
+  COWA_TRY(check_dq_ptrs(q, k, v, d_o, dq));
   COWA_TRY(check_device());
   if (s->n_qt == 0) return COWA_OK;
-  return hip_status(cowa::launch_bwd_dq(*p, cowa::sched_view(s), q, k, v, lse, d_o, dq, dsum,
+  return hip_status(cowa::launch_bwd_dq(*p, cowa::sched_view(s), q, k, v, d_o, dq, w,
                                         static_cast<hipStream_t>(stream)),
                     "backward dQ launch");
 }
@@ -592,22 +591,22 @@ cowa_status cowa_bwd(const cowa_params* p, const cowa_schedule_t* s, const void*
   COWA_TRY(check_params(p));
   Layout L;
   COWA_TRY(resolve_layout(p, &L));
-  float* dsum;
-  COWA_TRY(check_bwd(p, L, ws_bytes, workspace, &dsum));
+  cowa::BwdWork w;
+  COWA_TRY(check_bwd(p, L, ws_bytes, workspace, &w));
   COWA_TRY(check_schedule(p, L, s));
   if (no_work(p)) return COWA_OK;
-  COWA_TRY(check_prepare_ptrs(o, d_o));
-  COWA_TRY(check_main_ptrs(q, k, v, lse, d_o, dk, dv));
-  COWA_TRY(check_dq_ptrs(q, k, v, lse, d_o, dq));
+  COWA_TRY(check_prepare_ptrs(o, d_o, lse));
+  COWA_TRY(check_main_ptrs(q, k, v, d_o, dk, dv));
+  COWA_TRY(check_dq_ptrs(q, k, v, d_o, dq));
   COWA_TRY(check_device());
   hipStream_t st = static_cast<hipStream_t>(stream);
   const cowa::SchedView sv = cowa::sched_view(s);
   if (cowa::q_rows(*p) > 0)
-    COWA_TRY(hip_status(cowa::launch_bwd_prepare(*p, o, d_o, dsum, st), "backward prepare launch"));
+    COWA_TRY(hip_status(cowa::launch_bwd_prepare(*p, o, d_o, lse, w, st), "backward prepare launch"));
   if (s->n_kt > 0)
-    COWA_TRY(hip_status(cowa::launch_bwd_main(*p, sv, q, k, v, lse, d_o, dk, dv, dsum, st), "backward dK/dV launch"));
+    COWA_TRY(hip_status(cowa::launch_bwd_main(*p, sv, q, k, v, d_o, dk, dv, w, st), "backward dK/dV launch"));
   if (s->n_qt == 0) return COWA_OK;
-  return hip_status(cowa::launch_bwd_dq(*p, sv, q, k, v, lse, d_o, dq, dsum, st), "backward dQ launch");
+  return hip_status(cowa::launch_bwd_dq(*p, sv, q, k, v, d_o, dq, w, st), "backward dQ launch");
 }
 
 cowa_status cowa_decode_workspace_size(const cowa_decode_params* p, size_t* bytes) {

@@ -34,10 +34,14 @@ namespace {
 
 
 
-// D[row] = sum_d O[row, d] dO[row, d], D/8 lanes per row.
+// Per query row: nd = -D with D = sum_d O[row, d] dO[row, d] (D/8 lanes per
+// row), and nl = -LSE log2(e), the row's exponent offset in base 2; the dK/dV
+// pass folds nd into the accumulator input of dP = dO V^T (dP - D comes out of
+// the products) and adds nl to the scaled scores.
 template <int D>
 __global__ void __launch_bounds__(256) bwd_pre(const __bf16* __restrict__ o, const __bf16* __restrict__ d_o,
-                                               float* __restrict__ dsum, int64_t rows) {
+                                               const float* __restrict__ lse, float* __restrict__ nd,
+                                               float* __restrict__ nl, int64_t rows) {
   constexpr int CH = D / 8;
   const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t row = c / CH;
@@ -55,7 +59,10 @@ __global__ void __launch_bounds__(256) bwd_pre(const __bf16* __restrict__ o, con
   }
 #pragma unroll
   for (int off = 1; off < CH; off <<= 1) part += __shfl_xor(part, off);
-  if (row < rows && ch == 0) dsum[row] = part;
+  if (row < rows && ch == 0) {
+    nd[row] = -part;
+    nl[row] = -lse[row] * kLog2e;
+  }
 }
 
 template <int D, int BK, int NW_ = 4>
@@ -90,8 +97,8 @@ struct BwdCfg {
 template <int D, int BK, int NW>
 __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv, const __bf16* __restrict__ q,
                                                 const __bf16* __restrict__ k, const __bf16* __restrict__ v,
-                                                const __bf16* __restrict__ d_o, const float* __restrict__ lse,
-                                                const float* __restrict__ dsum, __bf16* __restrict__ dk,
+                                                const __bf16* __restrict__ d_o, const float* __restrict__ nl,
+                                                const float* __restrict__ nd, __bf16* __restrict__ dk,
                                                 __bf16* __restrict__ dv) {
   using C = BwdCfg<D, BK, NW>;
   extern __shared__ __align__(1024) unsigned char smem[];
@@ -203,7 +210,7 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
     const uint32_t bytes = (uint32_t)(n_q - q0) * D * 2;
     const int r = q0 + lane;
     const int rc = r < n_q ? r : n_q - 1;
-    return StageSrc{(row_base + q0) * D * 2, bytes, ((wave & 1) ? dsum : lse) + row_base + rc};
+    return StageSrc{(row_base + q0) * D * 2, bytes, ((wave & 1) ? nd : nl) + row_base + rc};
   };
   auto stage_piece = [&](const StageSrc& src, int n, int slot) {
     const unsigned char* qb = reinterpret_cast<const unsigned char*>(q) + src.off;
@@ -285,12 +292,13 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
     fa = ld_row8(qs + offr[ks] + mt * 16 * D * 2);
     fb = ld_row8(dos + offr[ks] + mt * 16 * D * 2);
   };
-  auto sdp_mfma = [&](int hf, int gi, const bf16x8& fa, const bf16x8& fb) {
+  // (dP accumulates on top of -D of its rows, so it holds dP - D)
+  auto sdp_mfma = [&](int hf, int gi, const bf16x8& fa, const bf16x8& fb, const f32x4 (&nd4)[C::MTQ]) {
     const int ks = gi >> 1, mt = 2 * hf + (gi & 1);
 #pragma unroll
     for (int nt = 0; nt < C::NTK; ++nt) {
       sacc[mt][nt] = mfma16(fa, kf[nt][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sacc[mt][nt]);
-      pacc[mt][nt] = mfma16(fb, vf[nt][ks], ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : pacc[mt][nt]);
+      pacc[mt][nt] = mfma16(fb, vf[nt][ks], ks == 0 ? nd4[mt] : pacc[mt][nt]);
     }
   };
   // dV/dK group md of half hf: d tile md, queries of the half as k-slots
@@ -312,24 +320,24 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
   // (2 hf + i) * 16 + 4 lg + r.  In a partial block the masked pairs get P = 0
   // through a -inf exponent, selected after the exponent has read the MFMA result.
   constexpr int EPC = 8 * C::NTK / NG;
-  auto soft_chunk = [&](int hf, int ci, const float4 (&l4)[2], const float4 (&d4)[2], bool masked, int q0) {
+  // (the row values are nl = -LSE log2(e), so x = S c + nl = (S - LSE) log2(e);
+  // pacc already holds dP - D)
+  auto soft_chunk = [&](int hf, int ci, const float4 (&l4)[2], bool masked, int q0) {
 #pragma unroll
     for (int jj = 0; jj < EPC; ++jj) {
       const int e = ci * EPC + jj, r = e & 3, nt = (e >> 2) % C::NTK, i = e / (4 * C::NTK), mt = 2 * hf + i;
       const float lv = r == 0 ? l4[i].x : r == 1 ? l4[i].y : r == 2 ? l4[i].z : l4[i].w;
-      const float dd = r == 0 ? d4[i].x : r == 1 ? d4[i].y : r == 2 ? d4[i].z : d4[i].w;
-      float x = fmaf(sacc[mt][nt][r], c, -lv * kLog2e);
+      float x = fmaf(sacc[mt][nt][r], c, lv);
       // (a row of a full block has a finite LSE; a masked pair may have LSE = -inf)
       if (masked) x = legal32(g, q0 + 4 * lg + mt * 16 + r, k0 + nt * 16) ? x : -INFINITY;
       const float pv = __builtin_amdgcn_exp2f(x);
       pb[hf][nt][4 * i + r] = (__bf16)pv;
-      sb[hf][nt][4 * i + r] = (__bf16)(pv * (pacc[mt][nt][r] - dd));
+      sb[hf][nt][4 * i + r] = (__bf16)(pv * pacc[mt][nt][r]);
     }
   };
-  // LSE and D of query tile 2 hf + i (the lane's rows 4 lg .. 4 lg + 3)
-  auto load_rowv = [&](const float* rowv, int hf, int i, float4 (&l4)[2], float4 (&d4)[2]) {
+  // nl of query tile 2 hf + i (the lane's rows 4 lg .. 4 lg + 3)
+  auto load_rowv = [&](const float* rowv, int hf, int i, float4 (&l4)[2]) {
     l4[i] = *reinterpret_cast<const float4*>(rowv + (2 * hf + i) * 16 + 4 * lg);
-    d4[i] = *reinterpret_cast<const float4*>(rowv + C::BQ + (2 * hf + i) * 16 + 4 * lg);
   };
 
   int slot = 0;  // ring slot of the step being computed (t mod 3)
@@ -356,7 +364,10 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
         dvdk_load(qs, dos, 1, gg - 3 * NG, fa, fb);
     };
     bf16x8 fa[PD + 1], fb[PD + 1];
-    float4 l4[2], d4[2];  // LSE and D of the half in the softmax
+    float4 l4[2];  // nl of the half in the softmax
+    f32x4 nd4[C::MTQ];  // -D of the step's rows, the accumulator input of dP
+#pragma unroll
+    for (int mt = 0; mt < C::MTQ; ++mt) nd4[mt] = *reinterpret_cast<const f32x4*>(rowv + C::BQ + mt * 16 + 4 * lg);
 #pragma unroll
     for (int gg = 0; gg < PD; ++gg) load_group(gg, fa[gg], fb[gg]);
     __builtin_amdgcn_sched_barrier(0);
@@ -369,23 +380,23 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
       // its softmax chunks [0, NG/2) and [NG/2, NG); each is loaded once the
       // previous half no longer reads that register
       if (gg == NG - 2) {
-        load_rowv(rowv, 0, 0, l4, d4);
-        load_rowv(rowv, 0, 1, l4, d4);
+        load_rowv(rowv, 0, 0, l4);
+        load_rowv(rowv, 0, 1, l4);
       }
-      if (gg == NG + NG / 2) load_rowv(rowv, 1, 0, l4, d4);
-      if (gg == 2 * NG) load_rowv(rowv, 1, 1, l4, d4);
+      if (gg == NG + NG / 2) load_rowv(rowv, 1, 0, l4);
+      if (gg == 2 * NG) load_rowv(rowv, 1, 1, l4);
       bf16x8& a0 = fa[gg % (PD + 1)];
       bf16x8& b0 = fb[gg % (PD + 1)];
       if (gg < NG)
-        sdp_mfma(0, gg, a0, b0);
+        sdp_mfma(0, gg, a0, b0, nd4);
       else if (gg < 2 * NG)
-        sdp_mfma(1, gg - NG, a0, b0);
+        sdp_mfma(1, gg - NG, a0, b0, nd4);
       else if (gg < 3 * NG)
         dvdk_mfma(0, gg - 2 * NG, a0, b0);
       else
         dvdk_mfma(1, gg - 3 * NG, a0, b0);
-      if (gg >= NG && gg < 2 * NG) soft_chunk(0, gg - NG, l4, d4, masked, q0);
-      if (gg >= 2 * NG && gg < 3 * NG) soft_chunk(1, gg - 2 * NG, l4, d4, masked, q0);
+      if (gg >= NG && gg < 2 * NG) soft_chunk(0, gg - NG, l4, masked, q0);
+      if (gg >= 2 * NG && gg < 3 * NG) soft_chunk(1, gg - 2 * NG, l4, masked, q0);
       __builtin_amdgcn_sched_barrier(0);
     }
 
@@ -447,7 +458,7 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
 
 template <int D, int BK, int NW = 4>
 hipError_t launch_main(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
-                       const void* d_o, const float* lse, const float* dsum, void* dk, void* dv,
+                       const void* d_o, const float* nl, const float* nd, void* dk, void* dv,
                        hipStream_t stream) {
   using C = BwdCfg<D, BK, NW>;
   static_assert(C::OUT_BYTES <= C::LDS_MAX && C::MAIN_BYTES < C::LDS_MAX, "LDS budget");
@@ -460,7 +471,7 @@ hipError_t launch_main(const cowa_params& p, const SchedView& sv, const void* q,
   const unsigned blocks = (unsigned)sv.n_kt * p.h_k * (sv.ragged ? 1 : p.batch);
   hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * NW), C::lds_bytes(sv.max_qt), stream, p, sv,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), static_cast<const __bf16*>(v),
-                     static_cast<const __bf16*>(d_o), lse, dsum, static_cast<__bf16*>(dk),
+                     static_cast<const __bf16*>(d_o), nl, nd, static_cast<__bf16*>(dk),
                      static_cast<__bf16*>(dv));
   return hipGetLastError();
 }
@@ -498,7 +509,7 @@ template <int D, int BQ, int BK, int NQW, bool W4>
 __global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, SchedView sv, int hpw,
                                                      const __bf16* __restrict__ q, const __bf16* __restrict__ k,
                                                      const __bf16* __restrict__ v, const __bf16* __restrict__ d_o,
-                                                     const float* __restrict__ lse, const float* __restrict__ dsum,
+                                                     const float* __restrict__ nl, const float* __restrict__ nd,
                                                      __bf16* __restrict__ dq) {
   using C = DqCfg<D, BQ, BK, NQW>;
   using T = typename C::T;
@@ -593,9 +604,10 @@ __global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, S
       qf[nt][ks] = ok ? a : bf16x8{};
       gf[nt][ks] = ok ? c2 : bf16x8{};
     }
-    const float lv = ok ? lse[row] : -INFINITY;
-    l2[nt] = lv == -INFINITY ? INFINITY : lv * kLog2e;
-    dd[nt] = ok ? dsum[row] : 0.f;
+    // nl = -LSE log2(e); a row without keys (LSE = -inf) or past n_q gets +inf, so P = 0
+    const float nlv = ok ? nl[row] : INFINITY;
+    l2[nt] = nlv == INFINITY ? INFINITY : -nlv;
+    dd[nt] = ok ? -nd[row] : 0.f;
   }
 
   f32x4 qacc[MTD][NTQ];  // dQ^T / scale: rows d, columns queries
@@ -735,7 +747,7 @@ __global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, S
 
 template <int D, int BQ, int BK, int NQW, bool W4>
 hipError_t launch_dq_w(const cowa_params& p, const SchedView& sv, int hpw, int waves, const void* q, const void* k,
-                       const void* v, const void* d_o, const float* lse, const float* dsum, void* dq,
+                       const void* v, const void* d_o, const float* nl, const float* nd, void* dq,
                        hipStream_t stream) {
   using C = DqCfg<D, BQ, BK, NQW>;
   auto kern = bwd_dq_kernel<D, BQ, BK, NQW, W4>;
@@ -747,21 +759,21 @@ hipError_t launch_dq_w(const cowa_params& p, const SchedView& sv, int hpw, int w
   const unsigned blocks = (unsigned)sv.n_qt * n_hgroups * (sv.ragged ? 1 : p.batch);
   hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * waves), C::lds_bytes(sv.max_kt), stream, p, sv, hpw,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), static_cast<const __bf16*>(v),
-                     static_cast<const __bf16*>(d_o), lse, dsum, static_cast<__bf16*>(dq));
+                     static_cast<const __bf16*>(d_o), nl, nd, static_cast<__bf16*>(dq));
   return hipGetLastError();
 }
 
 template <int D, int BQ, int BK, int NQW = 64>
 hipError_t launch_dq(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
-                     const void* d_o, const float* lse, const float* dsum, void* dq, hipStream_t stream) {
+                     const void* d_o, const float* nl, const float* nd, void* dq, hipStream_t stream) {
   using C = DqCfg<D, BQ, BK, NQW>;
   if (sv.max_kt > C::max_kblocks()) return hipErrorInvalidValue;
   const int G = p.h_q / p.h_k;
   int hpw = 256 / BQ;  // up to 256 query rows per workgroup
   while (hpw > 1 && G % hpw != 0) hpw >>= 1;
   const int waves = hpw * C::WPH;
-  if (waves == 4) return launch_dq_w<D, BQ, BK, NQW, true>(p, sv, hpw, waves, q, k, v, d_o, lse, dsum, dq, stream);
-  return launch_dq_w<D, BQ, BK, NQW, false>(p, sv, hpw, waves, q, k, v, d_o, lse, dsum, dq, stream);
+  if (waves == 4) return launch_dq_w<D, BQ, BK, NQW, true>(p, sv, hpw, waves, q, k, v, d_o, nl, nd, dq, stream);
+  return launch_dq_w<D, BQ, BK, NQW, false>(p, sv, hpw, waves, q, k, v, d_o, nl, nd, dq, stream);
 }
 
 }  // namespace
@@ -781,34 +793,33 @@ bool bwd_bf16_supported(int d, int tq, int tk) {
   return (d == 64 || d == 128) && (tq == 64 || tq == 128) && (tk == 64 || tk == 128);
 }
 
-hipError_t launch_bwd_prepare(const cowa_params& p, const void* o, const void* d_o, float* dsum,
-                              hipStream_t stream) {
+hipError_t launch_bwd_prepare(const cowa_params& p, const void* o, const void* d_o, const float* lse,
+                              const BwdWork& w, hipStream_t stream) {
   const int64_t rows = q_rows(p);
   const int64_t chunks = rows * (p.head_dim / 8);
   const unsigned blocks = (unsigned)((chunks + 255) / 256);
   if (p.head_dim == 128)
     hipLaunchKernelGGL(bwd_pre<128>, dim3(blocks), dim3(256), 0, stream, static_cast<const __bf16*>(o),
-                       static_cast<const __bf16*>(d_o), dsum, rows);
+                       static_cast<const __bf16*>(d_o), lse, w.nd, w.nl, rows);
   else
     hipLaunchKernelGGL(bwd_pre<64>, dim3(blocks), dim3(256), 0, stream, static_cast<const __bf16*>(o),
-                       static_cast<const __bf16*>(d_o), dsum, rows);
+                       static_cast<const __bf16*>(d_o), lse, w.nd, w.nl, rows);
   return hipGetLastError();
 }
 
 hipError_t launch_bwd_main(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
-                           const float* lse, const void* d_o, void* dk, void* dv, const float* dsum,
-                           hipStream_t stream) {
-  if (p.head_dim == 128 && p.tile_k == 128) return launch_main<128, 128>(p, sv, q, k, v, d_o, lse, dsum, dk, dv, stream);
-  if (p.head_dim == 128 && p.tile_k == 64) return launch_main<128, 64>(p, sv, q, k, v, d_o, lse, dsum, dk, dv, stream);
-  if (p.head_dim == 64 && p.tile_k == 128) return launch_main<64, 128>(p, sv, q, k, v, d_o, lse, dsum, dk, dv, stream);
-  if (p.head_dim == 64 && p.tile_k == 64) return launch_main<64, 64>(p, sv, q, k, v, d_o, lse, dsum, dk, dv, stream);
+                           const void* d_o, void* dk, void* dv, const BwdWork& w, hipStream_t stream) {
+  if (p.head_dim == 128 && p.tile_k == 128) return launch_main<128, 128>(p, sv, q, k, v, d_o, w.nl, w.nd, dk, dv, stream);
+  if (p.head_dim == 128 && p.tile_k == 64) return launch_main<128, 64>(p, sv, q, k, v, d_o, w.nl, w.nd, dk, dv, stream);
+  if (p.head_dim == 64 && p.tile_k == 128) return launch_main<64, 128>(p, sv, q, k, v, d_o, w.nl, w.nd, dk, dv, stream);
+  if (p.head_dim == 64 && p.tile_k == 64) return launch_main<64, 64>(p, sv, q, k, v, d_o, w.nl, w.nd, dk, dv, stream);
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_bwd_dq(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
-                         const float* lse, const void* d_o, void* dq, const float* dsum, hipStream_t stream) {
+                         const void* d_o, void* dq, const BwdWork& w, hipStream_t stream) {
 #define COWA_DQ_CASE(D_, BQ_, BK_) \
-  if (p.head_dim == D_ && p.tile_q == BQ_ && p.tile_k == BK_) return launch_dq<D_, BQ_, BK_>(p, sv, q, k, v, d_o, lse, dsum, dq, stream);
+  if (p.head_dim == D_ && p.tile_q == BQ_ && p.tile_k == BK_) return launch_dq<D_, BQ_, BK_>(p, sv, q, k, v, d_o, w.nl, w.nd, dq, stream);
   COWA_DQ_CASE(128, 128, 128)
   COWA_DQ_CASE(128, 128, 64)
   COWA_DQ_CASE(128, 64, 128)

@@ -89,14 +89,28 @@ int bwd_dq_max_kblocks(int head_dim, int tile_k);
 hipError_t launch_fwd_bf16(const cowa_params& p, const SchedView& sv, const void* q, const void* k,
                            const void* v, void* o, float* lse, hipStream_t stream);
 
-// Backward stages (Alg. 2): D = rowsum(O * dO); the dK/dV pass; the dQ pass.
-hipError_t launch_bwd_prepare(const cowa_params& p, const void* o, const void* d_o, float* dsum,
-                              hipStream_t stream);
+// Backward workspace: per query row (layout of LSE), nd = -D with
+// D = rowsum(O * dO) (the term of Alg. 2), then nl = -LSE log2(e); each array
+// 256-byte aligned.
+struct BwdWork {
+  float* nd;
+  float* nl;
+};
+inline size_t bwd_array_bytes(const cowa_params& p) { return ((size_t)q_rows(p) * sizeof(float) + 255) & ~size_t(255); }
+inline BwdWork bwd_work(const cowa_params& p, void* ws) {
+  BwdWork w;
+  w.nd = static_cast<float*>(ws);
+  w.nl = reinterpret_cast<float*>(static_cast<char*>(ws) + bwd_array_bytes(p));
+  return w;
+}
+
+// Backward stages (Alg. 2): the row values; the dK/dV pass; the dQ pass.
+hipError_t launch_bwd_prepare(const cowa_params& p, const void* o, const void* d_o, const float* lse,
+                              const BwdWork& w, hipStream_t stream);
 hipError_t launch_bwd_main(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
-                           const float* lse, const void* d_o, void* dk, void* dv, const float* dsum,
-                           hipStream_t stream);
+                           const void* d_o, void* dk, void* dv, const BwdWork& w, hipStream_t stream);
 hipError_t launch_bwd_dq(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
-                         const float* lse, const void* d_o, void* dq, const float* dsum, hipStream_t stream);
+                         const void* d_o, void* dq, const BwdWork& w, hipStream_t stream);
 
 bool decode_supported(int head_dim, int group);
 size_t decode_workspace_bytes(const cowa_decode_params& p);

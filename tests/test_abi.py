@@ -183,7 +183,7 @@ def test_bwd_workspace_and_errors_on_host():
     p = _good()
     need = abi.cowa_bwd_workspace_size(p)
     rows = p.batch * p.h_q * p.n_q
-    assert need >= rows * 4
+    assert need >= rows * 8
     p32 = _good()
     p32.dtype = abi.COWA_FP32
     s = _sized(p32)
@@ -247,7 +247,7 @@ def test_bwd_shape_limits_on_host(n_q, n_k, ok):
     assert st == abi.COWA_OK
     s = abi.cowa_schedule_t()
     vp = ctypes.c_void_p
-    st = lib.cowa_bwd_main(ctypes.byref(p), ctypes.byref(s), *[vp(1 << 24)] * 7, vp(1 << 24), need, vp(0))
+    st = lib.cowa_bwd_main(ctypes.byref(p), ctypes.byref(s), *[vp(1 << 24)] * 7, need, vp(0))
     if ok:
         assert st != abi.COWA_ERR_UNSUPPORTED
     else:
@@ -270,7 +270,7 @@ def test_bwd_checks_every_stage_before_any_launch():
     assert st == abi.COWA_ERR_UNSUPPORTED
     assert b"query blocks" in lib.cowa_last_error()
     # each stage on its own applies the same check
-    st = lib.cowa_bwd_main(ctypes.byref(p), ctypes.byref(s), *[vp(1 << 24)] * 8, ctypes.c_size_t(need), vp(0))
+    st = lib.cowa_bwd_main(ctypes.byref(p), ctypes.byref(s), *[vp(1 << 24)] * 7, ctypes.c_size_t(need), vp(0))
     assert st == abi.COWA_ERR_UNSUPPORTED
 
 
