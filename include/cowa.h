@@ -204,7 +204,12 @@ cowa_status cowa_fwd(const cowa_params* p, const cowa_schedule_t* s,
 
 /* Workspace bytes cowa_bwd needs: per query row, the float32 -D with
  * D = rowsum(O * dO) (the term of Alg. 2) and -LSE log2(e) (the row's
- * exponent offset in base 2): two arrays in the row layout of LSE. */
+ * exponent offset in base 2): two arrays in the row layout of LSE; then, when
+ * the KV blocks holding sink keys have query lists much longer than every
+ * other KV block (every query sees the sink, Eq. fwa_support), float32 dK/dV
+ * partials of those blocks, which the dK/dV stage walks in several parts and
+ * sums in a fixed order (at most 16 parts per block and 256 MB in total; the
+ * split depends only on the parameters, so results stay deterministic). */
 cowa_status cowa_bwd_workspace_size(const cowa_params* p, size_t* bytes);
 
 /* Backward (Alg. 2): exact gradients of <dO, O> w.r.t. the unscaled Q, K and

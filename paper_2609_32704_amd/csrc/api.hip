@@ -3,6 +3,7 @@
 // writes nothing.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <cmath>
 #include <cstdarg>
@@ -183,6 +184,47 @@ cowa::HeadGeo geo_of(const cowa_params* p, const Layout& L, int b, int h) {
 }
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Split plan of the dK/dV pass (cowa::BwdSplit): the leading KV blocks that hold
+// sink keys of some head are split into P parts, P = ceil(longest such column /
+// longest other column) (at most 16, and at most 256 MB of partials).  A
+// column past the sink holds at most the query blocks of its near run
+// (B_k + w_near - 1 distance-0 keys) and of its long-range run
+// (B_k + hi - lo - 1), each spanning up to one block more than its length.
+cowa::BwdSplit bwd_split_plan(const cowa_params* p, const Layout& L) {
+  cowa::BwdSplit sp;
+  if (p->tile_q < 1 || p->tile_k < 1 || L.max_kt == 0) return sp;
+  int64_t S = 0;
+  for (const cowa::WinDesc& w : L.win) S = std::max<int64_t>(S, ((int64_t)w.sink + p->tile_k - 1) / p->tile_k);
+  S = std::min<int64_t>(S, L.max_kt);
+  if (S == 0) return sp;
+  int64_t l_sink = 0, l_other = 1;
+  for (size_t b = 0; b < L.seq.size(); ++b) {
+    const int64_t bq = ((int64_t)L.seq[b].n_q + p->tile_q - 1) / p->tile_q;
+    const int64_t bk = ((int64_t)L.seq[b].n_k + p->tile_k - 1) / p->tile_k;
+    for (int h = 0; h < p->h_k; ++h) {
+      const cowa::HeadGeo g = geo_of(p, L, (int)b, h);
+      for (int64_t j = 0; j < std::min(S, bk); ++j)
+        l_sink = std::max<int64_t>(l_sink, cowa::ranges_count(cowa::bwd_block_ranges(g, (int32_t)j)));
+      const int64_t near = std::min<int64_t>(g.w_near, g.n_k), width = std::min<int64_t>(g.hi, g.n_k) -
+                                                                         std::min<int64_t>(g.lo, g.n_k);
+      int64_t other = 0;
+      if (near > 0) other += (p->tile_k + near - 2) / p->tile_q + 2;
+      if (width > 0) other += (p->tile_k + width - 2) / p->tile_q + 2;
+      l_other = std::max(l_other, std::min(bq, other));
+    }
+  }
+  const int64_t seqs = L.ragged ? (int64_t)L.seq.size() : p->batch;
+  int64_t P = std::min<int64_t>((l_sink + l_other - 1) / l_other, 16);
+  const size_t col_bytes = cowa::bwd_part_floats(*p) * sizeof(float);
+  while (P > 1 && (size_t)(seqs * p->h_k * S * P) * col_bytes > (size_t(256) << 20)) --P;
+  if (P <= 1) return sp;
+  sp.S = (int32_t)S;
+  sp.P = (int32_t)P;
+  sp.n_cols = seqs * p->h_k * S;
+  return sp;
+}
+
 
 // Every schedule-relevant field must match (the digest covers windows and lengths).
 bool same_schedule(const cowa_params* a, const cowa_params* b) {
@@ -476,7 +518,9 @@ cowa_status cowa_fwd(const cowa_params* p, const cowa_schedule_t* s, const void*
 cowa_status cowa_bwd_workspace_size(const cowa_params* p, size_t* bytes) {
   COWA_TRY(check_params(p));
   if (!bytes) return fail(COWA_ERR_INVALID_ARG, "bytes is NULL");
-  *bytes = 2 * cowa::bwd_array_bytes(*p);
+  Layout L;
+  COWA_TRY(resolve_layout(p, &L));
+  *bytes = cowa::bwd_workspace_bytes(*p, bwd_split_plan(p, L));
   return COWA_OK;
 }
 
@@ -500,11 +544,13 @@ static cowa_status check_bwd(const cowa_params* p, const Layout& L, size_t ws_by
     return fail(COWA_ERR_UNSUPPORTED, "too many key blocks for one launch");
   if ((int64_t)L.n_qt * p->h_q * seq_factor(p) >= (int64_t(1) << 31))
     return fail(COWA_ERR_UNSUPPORTED, "too many query blocks for one launch");
-  size_t need = 0;
-  COWA_TRY(cowa_bwd_workspace_size(p, &need));
+  const cowa::BwdSplit sp = bwd_split_plan(p, L);
+  if ((int64_t)L.n_kt * p->h_k * seq_factor(p) + sp.n_cols * sp.P + 8 >= (int64_t(1) << 31))
+    return fail(COWA_ERR_UNSUPPORTED, "too many key blocks for one launch");
+  const size_t need = cowa::bwd_workspace_bytes(*p, sp);
   if (!no_work(p) && (!workspace || ws_bytes < need || !aligned(workspace, 256)))
     return fail(COWA_ERR_WORKSPACE, "backward needs a 256-byte aligned workspace of %zu bytes (got %zu)", need, ws_bytes);
-  *w = cowa::bwd_work(*p, workspace);
+  *w = cowa::bwd_work(*p, sp, workspace);
   return COWA_OK;
 }
 

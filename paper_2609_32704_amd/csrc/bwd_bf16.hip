@@ -94,8 +94,19 @@ struct BwdCfg {
   static int max_qblocks() { return (LDS_MAX - MAIN_BYTES) / 4; }
 };
 
+// Parts of the split columns (BwdSplit): the first n_extra workgroups (a
+// multiple of 8, so the XCD order of the others is unchanged) take parts
+// 1 .. P-1 of the first S KV blocks of every (sequence, KV head); the other
+// workgroups take one column each (part 0 of a split column).
+struct SplitArgs {
+  float* part;       // [split column][P][2][BK * D] float32 partials
+  int32_t S, P;      // split blocks per (sequence, KV head); parts (1: no split)
+  int32_t n_extra;   // workgroups of parts 1 .. P-1, rounded up to a multiple of 8
+};
+
 template <int D, int BK, int NW>
-__global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv, const __bf16* __restrict__ q,
+__global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv, SplitArgs sa,
+                                                const __bf16* __restrict__ q,
                                                 const __bf16* __restrict__ k, const __bf16* __restrict__ v,
                                                 const __bf16* __restrict__ d_o, const float* __restrict__ nl,
                                                 const float* __restrict__ nd, __bf16* __restrict__ dk,
@@ -105,10 +116,32 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
 
   // clusters of 32 consecutive KV blocks of one KV head share an XCD's L2;
   // first blocks (the sink, with the longest query lists) first
-  const WorkItem wi = cluster_item(blockIdx.x, sv.n_kt, 1, grid_units(p, sv), 32, false);
+  int part = 0;
+  WorkItem wi;
+  if ((int)blockIdx.x < sa.n_extra) {
+    const int e = blockIdx.x;
+    part = 1 + e % (sa.P - 1);
+    const int rest = e / (sa.P - 1);
+    const int tile = rest % sa.S, us = rest / sa.S;  // us = sequence * h_k + KV head
+    if (us >= p.batch * p.h_k) return;               // padding
+    wi.group = 0;
+    if (!sv.ragged) {
+      wi.row = tile;
+      wi.unit = us;
+    } else {
+      const SeqDesc sd = sv.seq[us / p.h_k];
+      if (tile * BK >= sd.n_k) return;  // a sequence with fewer blocks
+      wi.row = sd.kt_off + tile;
+      wi.unit = us % p.h_k;
+    }
+  } else {
+    wi = cluster_item(blockIdx.x - sa.n_extra, sv.n_kt, 1, grid_units(p, sv), 32, false);
+  }
   int hk;
   const SeqCtx sc = seq_ctx(p, sv, wi.row, wi.unit, false, hk);
   const int j = sc.tile;
+  const bool split = sa.P > 1 && j < sa.S;
+  const int n_parts = split ? sa.P : 1;
   const int G = p.h_q / p.h_k;
   const Geo32 g = sc.g;
   const int n_q = sc.n_q, n_k = sc.n_k;
@@ -149,10 +182,21 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
   const int n_part = n_ent - n_full;
   const int subs = p.tile_q / C::BQ;
   const int steps_full = G * n_full * subs, n_steps = G * n_ent * subs;
-  // cursor (phase: 0 full / 1 partial, QO head, list index, sub-block)
-  int c_ph = n_full > 0 ? 0 : 1, c_k = 0, c_sub = 0;  // step being computed
-  int n1_ph = c_ph, n1_hh = 0, n1_k = 0, n1_sub = 0;  // the next step (staged)
-  int n2_ph = c_ph, n2_hh = 0, n2_k = 0, n2_sub = 0;  // the step after (being staged)
+  // this workgroup's steps: all of them, or part `part` of n_parts contiguous shares
+  const int s_begin = (int)((int64_t)n_steps * part / n_parts);
+  const int s_end = (int)((int64_t)n_steps * (part + 1) / n_parts);
+  // cursor (phase: 0 full / 1 partial, QO head, list index, sub-block) of step s_begin
+  int c_ph, c_k, c_sub, c_hh;
+  {
+    c_ph = s_begin < steps_full ? 0 : 1;
+    const int r = c_ph ? s_begin - steps_full : s_begin;
+    const int nl_ = c_ph ? n_part : n_full;
+    c_hh = nl_ > 0 ? r / (nl_ * subs) : 0;
+    c_k = nl_ > 0 ? (r / subs) % nl_ : 0;
+    c_sub = r % subs;
+  }
+  int n1_ph = c_ph, n1_hh = c_hh, n1_k = c_k, n1_sub = c_sub;  // the next step (staged)
+  int n2_ph = c_ph, n2_hh = c_hh, n2_k = c_k, n2_sub = c_sub;  // the step after (being staged)
   auto advance = [&](int& ph, int& hh, int& kk, int& sub) {
     if (++sub == subs) {
       sub = 0;
@@ -232,9 +276,9 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
   for (int x = tid; x < 2 * C::NST * C::QT::BYTES / 16; x += blockDim.x)
     reinterpret_cast<uint4*>(smem)[x] = uint4{0u, 0u, 0u, 0u};
   __syncthreads();  // the entry lists and the zeroed stages are in LDS
-  // prologue: steps 0 and 1 in flight
-  if (n_steps > 0) {
-    stage(entry_of(n2_ph, n2_k), n2_hh, n2_sub, 0);  // step 0
+  // prologue: the first two steps in flight
+  if (s_end > s_begin) {
+    stage(entry_of(n2_ph, n2_k), n2_hh, n2_sub, 0);  // step s_begin
     advance(n2_ph, n2_hh, n2_k, n2_sub);
     n1_ph = n2_ph, n1_hh = n2_hh, n1_k = n2_k, n1_sub = n2_sub;
     stage(entry_of(n2_ph, n2_k), n2_hh, n2_sub, 1);  // step 1
@@ -422,15 +466,31 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
     advance(n2_ph, n2_hh, n2_k, n2_sub);
     slot = slot == 2 ? 0 : slot + 1;
   };
-  int t = 0;
-  for (; t < steps_full; ++t) step(false);
-  for (; t < n_steps; ++t) step(true);
+  int t = s_begin;
+  for (; t < (s_end < steps_full ? s_end : steps_full); ++t) step(false);
+  for (; t < s_end; ++t) step(true);
 
   // the copies staged past the last step must land before their LDS is reused
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  // write dK and dV of the block: through LDS as [key][d], then 16-byte rows
   const float scale = p.softmax_scale;
+  if (split) {
+    // float32 partials in register order: element ((md NTK + nt) NW + wave) 64 + lane
+    // holds rows d = 16 md + 4 (lane / 16) + 0..3, key wave NKW + 16 nt + lane % 16
+    const int64_t col = ((int64_t)(sc.b * p.h_k + hk) * sa.S + j) * sa.P + part;
+    f32x4* pk = reinterpret_cast<f32x4*>(sa.part + col * 2 * BK * D);
+    f32x4* pv = pk + BK * D / 4;
+#pragma unroll
+    for (int md = 0; md < C::MD; ++md)
+#pragma unroll
+      for (int nt = 0; nt < C::NTK; ++nt) {
+        const int x = ((md * C::NTK + nt) * NW + wave) * 64 + lane;
+        pk[x] = scale * dka[md][nt];
+        pv[x] = dva[md][nt];
+      }
+    return;
+  }
+  // write dK and dV of the block: through LDS as [key][d], then 16-byte rows
   __bf16* tk = reinterpret_cast<__bf16*>(smem);                        // [BK][D + 8]
   __bf16* tv = reinterpret_cast<__bf16*>(smem) + BK * (D + 8);         // [BK][D + 8]
 #pragma unroll
@@ -456,10 +516,55 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
   }
 }
 
+// Sum of the P partials of each split column (in part order) -> bf16 dK, dV;
+// one workgroup per split column, each thread the register-order elements a
+// lane of bwd_main held.
+template <int D, int BK, int NW>
+__global__ void __launch_bounds__(64 * NW) bwd_split_sum(cowa_params p, SchedView sv, SplitArgs sa,
+                                                     __bf16* __restrict__ dk, __bf16* __restrict__ dv) {
+  using C = BwdCfg<D, BK, NW>;
+  const int c = blockIdx.x;  // (sequence * h_k + KV head) * S + block
+  const int j = c % sa.S, us = c / sa.S, b = us / p.h_k, hk = us % p.h_k;
+  int n_k;
+  int64_t row0;  // row of key 0 of this (sequence, KV head) in K, V, dK, dV
+  if (!sv.ragged) {
+    n_k = p.n_k;
+    row0 = ((int64_t)b * p.h_k + hk) * p.n_k;
+  } else {
+    const SeqDesc sd = sv.seq[b];
+    n_k = sd.n_k;
+    row0 = (int64_t)hk * p.n_k + sd.k_start;
+  }
+  if (j * BK >= n_k) return;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const f32x4* src = reinterpret_cast<const f32x4*>(sa.part + (int64_t)c * sa.P * 2 * BK * D);
+#pragma unroll
+  for (int md = 0; md < C::MD; ++md)
+#pragma unroll
+    for (int nt = 0; nt < C::NTK; ++nt) {
+      const int x = ((md * C::NTK + nt) * NW + wave) * 64 + lane;
+      f32x4 a = src[x], g = src[BK * D / 4 + x];
+      for (int pt = 1; pt < sa.P; ++pt) {
+        a += src[pt * (2 * BK * D / 4) + x];
+        g += src[pt * (2 * BK * D / 4) + BK * D / 4 + x];
+      }
+      const int64_t kp = (int64_t)j * BK + wave * C::NKW + nt * 16 + lr;
+      if (kp >= n_k) continue;
+      bf16x4 ka, va;
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        ka[rr] = (__bf16)a[rr];
+        va[rr] = (__bf16)g[rr];
+      }
+      const int64_t off = (row0 + kp) * D + md * 16 + 4 * lg;
+      *reinterpret_cast<bf16x4*>(dk + off) = ka;
+      *reinterpret_cast<bf16x4*>(dv + off) = va;
+    }
+}
+
 template <int D, int BK, int NW = 4>
 hipError_t launch_main(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
-                       const void* d_o, const float* nl, const float* nd, void* dk, void* dv,
-                       hipStream_t stream) {
+                       const void* d_o, const BwdWork& w, void* dk, void* dv, hipStream_t stream) {
   using C = BwdCfg<D, BK, NW>;
   static_assert(C::OUT_BYTES <= C::LDS_MAX && C::MAIN_BYTES < C::LDS_MAX, "LDS budget");
   if (sv.max_qt > C::max_qblocks()) return hipErrorInvalidValue;
@@ -468,11 +573,19 @@ hipError_t launch_main(const cowa_params& p, const SchedView& sv, const void* q,
     const hipError_t err = allow_lds(reinterpret_cast<const void*>(kern), C::LDS_MAX);
     if (err != hipSuccess) return err;
   }
-  const unsigned blocks = (unsigned)sv.n_kt * p.h_k * (sv.ragged ? 1 : p.batch);
-  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * NW), C::lds_bytes(sv.max_qt), stream, p, sv,
+  SplitArgs sa;
+  sa.part = w.part;
+  sa.S = w.split.S;
+  sa.P = w.split.P;
+  sa.n_extra = sa.P > 1 ? (int32_t)(((int64_t)p.batch * p.h_k * sa.S * (sa.P - 1) + 7) / 8 * 8) : 0;
+  const unsigned blocks = (unsigned)sv.n_kt * p.h_k * (sv.ragged ? 1 : p.batch) + (unsigned)sa.n_extra;
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * NW), C::lds_bytes(sv.max_qt), stream, p, sv, sa,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), static_cast<const __bf16*>(v),
-                     static_cast<const __bf16*>(d_o), nl, nd, static_cast<__bf16*>(dk),
+                     static_cast<const __bf16*>(d_o), w.nl, w.nd, static_cast<__bf16*>(dk),
                      static_cast<__bf16*>(dv));
+  if (sa.P > 1)
+    hipLaunchKernelGGL((bwd_split_sum<D, BK, NW>), dim3((unsigned)w.split.n_cols), dim3(64 * NW), 0, stream, p, sv,
+                       sa, static_cast<__bf16*>(dk), static_cast<__bf16*>(dv));
   return hipGetLastError();
 }
 
@@ -809,10 +922,10 @@ hipError_t launch_bwd_prepare(const cowa_params& p, const void* o, const void* d
 
 hipError_t launch_bwd_main(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
                            const void* d_o, void* dk, void* dv, const BwdWork& w, hipStream_t stream) {
-  if (p.head_dim == 128 && p.tile_k == 128) return launch_main<128, 128>(p, sv, q, k, v, d_o, w.nl, w.nd, dk, dv, stream);
-  if (p.head_dim == 128 && p.tile_k == 64) return launch_main<128, 64>(p, sv, q, k, v, d_o, w.nl, w.nd, dk, dv, stream);
-  if (p.head_dim == 64 && p.tile_k == 128) return launch_main<64, 128>(p, sv, q, k, v, d_o, w.nl, w.nd, dk, dv, stream);
-  if (p.head_dim == 64 && p.tile_k == 64) return launch_main<64, 64>(p, sv, q, k, v, d_o, w.nl, w.nd, dk, dv, stream);
+  if (p.head_dim == 128 && p.tile_k == 128) return launch_main<128, 128>(p, sv, q, k, v, d_o, w, dk, dv, stream);
+  if (p.head_dim == 128 && p.tile_k == 64) return launch_main<128, 64>(p, sv, q, k, v, d_o, w, dk, dv, stream);
+  if (p.head_dim == 64 && p.tile_k == 128) return launch_main<64, 128>(p, sv, q, k, v, d_o, w, dk, dv, stream);
+  if (p.head_dim == 64 && p.tile_k == 64) return launch_main<64, 64>(p, sv, q, k, v, d_o, w, dk, dv, stream);
   return hipErrorInvalidValue;
 }
 

@@ -89,18 +89,45 @@ int bwd_dq_max_kblocks(int head_dim, int tile_k);
 hipError_t launch_fwd_bf16(const cowa_params& p, const SchedView& sv, const void* q, const void* k,
                            const void* v, void* o, float* lse, hipStream_t stream);
 
+// Split of the dK/dV pass's heaviest columns.  Every query that reaches a sink
+// key sees it, so the sink KV blocks have query lists as long as the sequence
+// while every other column holds only its near and long-range runs; walked by
+// one workgroup, a sink column would set the pass's length whenever the other
+// columns do not fill the device for longer (one KV head per device, short or
+// few sequences).  The first S KV blocks of every (sequence, KV head) are
+// therefore walked by P workgroups, each taking a contiguous share of the
+// column's steps and writing float32 partial dK and dV; a reduction kernel
+// sums the P partials of a column in a fixed order (deterministic) and writes
+// bf16.  P = 1: no split.
+struct BwdSplit {
+  int32_t S = 0, P = 1;  // leading KV blocks split per (sequence, KV head); parts per column
+  int64_t n_cols = 0;    // split columns: sequences x KV heads x S
+};
+// float32 partial bytes of a column part: dK and dV of one KV block
+inline size_t bwd_part_floats(const cowa_params& p) { return (size_t)2 * p.tile_k * p.head_dim; }
+
 // Backward workspace: per query row (layout of LSE), nd = -D with
-// D = rowsum(O * dO) (the term of Alg. 2), then nl = -LSE log2(e); each array
-// 256-byte aligned.
+// D = rowsum(O * dO) (the term of Alg. 2), then nl = -LSE log2(e); then the
+// float32 partials of the split dK/dV columns; each array 256-byte aligned.
 struct BwdWork {
   float* nd;
   float* nl;
+  float* part;  // [n_cols][P][2][tile_k * head_dim], or null when P = 1
+  BwdSplit split;
 };
 inline size_t bwd_array_bytes(const cowa_params& p) { return ((size_t)q_rows(p) * sizeof(float) + 255) & ~size_t(255); }
-inline BwdWork bwd_work(const cowa_params& p, void* ws) {
+inline size_t bwd_split_bytes(const cowa_params& p, const BwdSplit& s) {
+  return s.P > 1 ? (((size_t)s.n_cols * s.P * bwd_part_floats(p) * sizeof(float) + 255) & ~size_t(255)) : 0;
+}
+inline size_t bwd_workspace_bytes(const cowa_params& p, const BwdSplit& s) {
+  return 2 * bwd_array_bytes(p) + bwd_split_bytes(p, s);
+}
+inline BwdWork bwd_work(const cowa_params& p, const BwdSplit& s, void* ws) {
   BwdWork w;
   w.nd = static_cast<float*>(ws);
   w.nl = reinterpret_cast<float*>(static_cast<char*>(ws) + bwd_array_bytes(p));
+  w.part = s.P > 1 ? reinterpret_cast<float*>(static_cast<char*>(ws) + 2 * bwd_array_bytes(p)) : nullptr;
+  w.split = s;
   return w;
 }
 
