@@ -329,24 +329,32 @@ def main():
             wsb = _abi.cowa_bwd_workspace_size(par)
             ws_ = torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
             tf = tb = 0.0
+            stages = [0.0, 0.0, 0.0]  # backward prepare, dK/dV pass, dQ pass
             for it in range(iters + 1):
-                e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+                e = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
                 e[0].record()
                 _abi.cowa_schedule(sch.s, stream)
                 _abi.cowa_fwd(par, sch.s, tq.data_ptr(), tk.data_ptr(), tv.data_ptr(), o_.data_ptr(),
                               lse_.data_ptr(), stream)
                 e[1].record()
-                _abi.cowa_bwd(par, sch.s, tq.data_ptr(), tk.data_ptr(), tv.data_ptr(), o_.data_ptr(), lse_.data_ptr(),
-                              tdo.data_ptr(), dq_.data_ptr(), dk_.data_ptr(), dv_.data_ptr(), ws_.data_ptr(), wsb,
-                              stream)
+                _abi.cowa_bwd_prepare(par, o_.data_ptr(), tdo.data_ptr(), lse_.data_ptr(), ws_.data_ptr(), wsb, stream)
                 e[2].record()
+                _abi.cowa_bwd_main(par, sch.s, tq.data_ptr(), tk.data_ptr(), tv.data_ptr(), tdo.data_ptr(),
+                                   dk_.data_ptr(), dv_.data_ptr(), ws_.data_ptr(), wsb, stream)
+                e[3].record()
+                _abi.cowa_bwd_dq(par, sch.s, tq.data_ptr(), tk.data_ptr(), tv.data_ptr(), tdo.data_ptr(),
+                                 dq_.data_ptr(), ws_.data_ptr(), wsb, stream)
+                e[4].record()
                 torch.cuda.synchronize()
                 if it:
                     tf += e[0].elapsed_time(e[1]) / iters
-                    tb += e[1].elapsed_time(e[2]) / iters
+                    tb += e[1].elapsed_time(e[4]) / iters
+                    for x in range(3):
+                        stages[x] += e[x + 1].elapsed_time(e[x + 2]) / iters
             pr = _abi.cowa_legal_pairs(par)
             d_ = par.head_dim
             return {"fwd_ms": tf, "bwd_ms": tb, "legal_pairs": pr,
+                    "bwd_prepare_ms": stages[0], "bwd_main_ms": stages[1], "bwd_dq_ms": stages[2],
                     "fwd_tflops": 4 * d_ * pr / (tf * 1e-3) / 1e12, "bwd_tflops": 10 * d_ * pr / (tb * 1e-3) / 1e12,
                     "fwd_frac": 4 * d_ * pr / (tf * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
                     "bwd_frac": 10 * d_ * pr / (tb * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}

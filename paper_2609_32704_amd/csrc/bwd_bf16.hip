@@ -931,6 +931,7 @@ hipError_t launch_bwd_main(const cowa_params& p, const SchedView& sv, const void
 
 hipError_t launch_bwd_dq(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
                          const void* d_o, void* dq, const BwdWork& w, hipStream_t stream) {
+  if (bwd_dq32_supported(p)) return launch_bwd_dq32(p, sv, q, k, v, d_o, dq, w, stream);
 #define COWA_DQ_CASE(D_, BQ_, BK_) \
   if (p.head_dim == D_ && p.tile_q == BQ_ && p.tile_k == BK_) return launch_dq<D_, BQ_, BK_>(p, sv, q, k, v, d_o, w.nl, w.nd, dq, stream);
   COWA_DQ_CASE(128, 128, 128)

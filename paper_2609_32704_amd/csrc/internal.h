@@ -138,6 +138,11 @@ hipError_t launch_bwd_main(const cowa_params& p, const SchedView& sv, const void
                            const void* d_o, void* dk, void* dv, const BwdWork& w, hipStream_t stream);
 hipError_t launch_bwd_dq(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
                          const void* d_o, void* dq, const BwdWork& w, hipStream_t stream);
+// the pipelined dQ pass on 32x32 products (128-key blocks, four-wave
+// workgroups); launch_bwd_dq uses it where supported
+bool bwd_dq32_supported(const cowa_params& p);
+hipError_t launch_bwd_dq32(const cowa_params& p, const SchedView& sv, const void* q, const void* k, const void* v,
+                           const void* d_o, void* dq, const BwdWork& w, hipStream_t stream);
 
 bool decode_supported(int head_dim, int group);
 size_t decode_workspace_bytes(const cowa_decode_params& p);

@@ -80,6 +80,9 @@ ODD = [
     # four-wave dQ workgroups of 64-row query blocks (4 QO heads each)
     ("gqa4_tq64", 1, 900, 900, 8, 2, 128, 8, 200, 64, 128, 0, 0),
     ("gqa4_d64_t64", 1, 650, 650, 4, 1, 64, 16, 130, 64, 64, 0, 0),
+    # the pipelined dQ pass (128-key blocks) at head dimension 64
+    ("gqa2_d64_t128", 1, 600, 600, 4, 2, 64, 8, 150, 128, 128, 0, 0),
+    ("gqa4_d64_tq64_t128", 1, 700, 700, 8, 2, 64, 8, 150, 64, 128, 0, 0),
 ]
 
 
