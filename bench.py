@@ -29,6 +29,11 @@ Extra blocks in the JSON line:
                 w_near = N), the in-house FullAttn twin, and CoWA/dense ratios
   cpu_baseline  the fp64 CPU oracle timed on a bounded sample of the same
                 workload on this host (with the host's CPU model and memory)
+  ceilings      what the device sustains outside this library: a 16384^3
+                bf16 GEMM through torch.matmul (hipBLASLt) and a 4 GiB device
+                copy and a read-only sum over it (torch's own kernels, which
+                reach less than the decoding kernel here); each matrix kernel
+                also reports its rate as a fraction of the GEMM
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
@@ -145,7 +150,8 @@ def main():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-workloads", action="store_true", help="skip the 8K / 32K / per-rank timings")
-    ap.add_argument("--only", choices=["all", "train", "decode", "copy"], default="all",
+    ap.add_argument("--no-ceiling", action="store_true", help="skip the vendor GEMM / copy reference timings")
+    ap.add_argument("--only", choices=["all", "train", "decode", "copy", "ceiling"], default="all",
                     help="profiling aid: run only part of the step (the JSON line is printed for 'all' only)")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -170,6 +176,57 @@ def main():
             out[s].copy_(torch.randn(shape[1:], generator=gen, device=dev, dtype=torch.float32))
         return out
 
+    def ceilings():
+        """What the device sustains outside this library: a bf16 GEMM through
+        torch.matmul (hipBLASLt) and a device-to-device copy, timed with HIP
+        events.  Under sustained matrix-core load the shader clock drops well
+        below its 2.4 GHz peak, so the vendor GEMM bounds what any bf16 kernel
+        reaches in practice."""
+        n = 16384
+        a = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+        b = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+        for _ in range(6):  # the shader clock settles over the first launches
+            c = a @ b
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(10):
+            c = a @ b
+        e1.record()
+        torch.cuda.synchronize()
+        gemm_ms = e0.elapsed_time(e1) / 10
+        del a, b, c
+        src = torch.empty(4 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(5):
+            dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        copy_ms = e0.elapsed_time(e1) / 5
+        del dst
+        x = src.view(torch.float32)
+        tot = x.sum()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(5):
+            tot = x.sum()
+        e1.record()
+        torch.cuda.synchronize()
+        read_ms = e0.elapsed_time(e1) / 5
+        del src, x, tot
+        return {"gemm_bf16_tflops": 2 * n ** 3 / (gemm_ms * 1e-3) / 1e12, "gemm_shape": f"{n}x{n}x{n}",
+                "copy_gbps": 2 * (4 << 30) / (copy_ms * 1e-3) / 1e9, "read_gbps": (4 << 30) / (read_ms * 1e-3) / 1e9,
+                "hbm_bytes": 4 << 30,
+                "note": "torch.matmul (hipBLASLt) bf16 GEMM (6 warm-up + 10 timed); a 4 GiB device copy (read + "
+                        "write bytes) and a float32 sum over the same 4 GiB (read bytes), 5 runs each"}
+
+    if args.only == "ceiling":
+        log("ceilings:", ceilings())
+        return
+
     if args.only == "copy":
         # plain device copy of a known size: the reference for HBM byte counters
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
@@ -180,6 +237,10 @@ def main():
         log("copied 3 x 1 GiB")
         return
 
+    ceil = None
+    if args.only == "all" and not args.no_ceiling:
+        log("vendor GEMM and copy reference timings")
+        ceil = ceilings()
     do_train = args.only in ("all", "train")
     do_decode = args.only in ("all", "decode")
     T = TRAIN
@@ -302,11 +363,17 @@ def main():
         elif kn["bound"] == "hbm":
             kn["frac"] = kn["achieved"] / PEAK_HBM_GBPS
 
+    if ceil:
+        for kn in kernels.values():
+            if kn["bound"] == "mfma":
+                kn["frac_of_gemm"] = kn["achieved"] / ceil["gemm_bf16_tflops"]
+
     main_k = kernels["bwd_main"]
     traffic = read_traffic("bwd_main")
     roofline = {"kernel": "bwd_main (backward dK/dV pass, 131072 tokens)", "bound": "mfma",
                 "achieved": main_k["achieved"], "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": main_k["frac"], "traffic": traffic,
+                "frac_of_gemm_ceiling": main_k.get("frac_of_gemm"),
                 "work_per_launch": f"{8 * T['d'] * pairs:.4e} FLOP = 8 d x {pairs} legal pairs"}
 
     # decode: counter bytes (both kernels) over the algorithmic bytes
@@ -435,6 +502,7 @@ def main():
         "decode_ms": per["decode"], "decode_gbps": dec_bytes / (per["decode"] * 1e-3) / 1e9,
         "legal_pairs": pairs, "decode_visible_keys": vis_keys,
         "roofline": roofline, "kernels": kernels, "workloads": workloads, "dense": dense, "cpu_baseline": cpu,
+        "ceilings": ceil,
     }
     print(json.dumps(out), flush=True)
 

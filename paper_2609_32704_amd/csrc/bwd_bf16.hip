@@ -517,8 +517,8 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
 }
 
 // Sum of the P partials of each split column (in part order) -> bf16 dK, dV;
-// one workgroup per split column, each thread the register-order elements a
-// lane of bwd_main held.
+// one workgroup per (split column, 16-row d tile), each thread the
+// register-order elements a lane of bwd_main held for that d tile.
 template <int D, int BK, int NW>
 __global__ void __launch_bounds__(64 * NW) bwd_split_sum(cowa_params p, SchedView sv, SplitArgs sa,
                                                      __bf16* __restrict__ dk, __bf16* __restrict__ dv) {
@@ -538,28 +538,27 @@ __global__ void __launch_bounds__(64 * NW) bwd_split_sum(cowa_params p, SchedVie
   if (j * BK >= n_k) return;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
   const f32x4* src = reinterpret_cast<const f32x4*>(sa.part + (int64_t)c * sa.P * 2 * BK * D);
+  const int md = blockIdx.y;
 #pragma unroll
-  for (int md = 0; md < C::MD; ++md)
-#pragma unroll
-    for (int nt = 0; nt < C::NTK; ++nt) {
-      const int x = ((md * C::NTK + nt) * NW + wave) * 64 + lane;
-      f32x4 a = src[x], g = src[BK * D / 4 + x];
-      for (int pt = 1; pt < sa.P; ++pt) {
-        a += src[pt * (2 * BK * D / 4) + x];
-        g += src[pt * (2 * BK * D / 4) + BK * D / 4 + x];
-      }
-      const int64_t kp = (int64_t)j * BK + wave * C::NKW + nt * 16 + lr;
-      if (kp >= n_k) continue;
-      bf16x4 ka, va;
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        ka[rr] = (__bf16)a[rr];
-        va[rr] = (__bf16)g[rr];
-      }
-      const int64_t off = (row0 + kp) * D + md * 16 + 4 * lg;
-      *reinterpret_cast<bf16x4*>(dk + off) = ka;
-      *reinterpret_cast<bf16x4*>(dv + off) = va;
+  for (int nt = 0; nt < C::NTK; ++nt) {
+    const int x = ((md * C::NTK + nt) * NW + wave) * 64 + lane;
+    f32x4 a = src[x], g = src[BK * D / 4 + x];
+    for (int pt = 1; pt < sa.P; ++pt) {
+      a += src[pt * (2 * BK * D / 4) + x];
+      g += src[pt * (2 * BK * D / 4) + BK * D / 4 + x];
     }
+    const int64_t kp = (int64_t)j * BK + wave * C::NKW + nt * 16 + lr;
+    if (kp >= n_k) continue;
+    bf16x4 ka, va;
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      ka[rr] = (__bf16)a[rr];
+      va[rr] = (__bf16)g[rr];
+    }
+    const int64_t off = (row0 + kp) * D + md * 16 + 4 * lg;
+    *reinterpret_cast<bf16x4*>(dk + off) = ka;
+    *reinterpret_cast<bf16x4*>(dv + off) = va;
+  }
 }
 
 template <int D, int BK, int NW = 4>
@@ -584,7 +583,7 @@ hipError_t launch_main(const cowa_params& p, const SchedView& sv, const void* q,
                      static_cast<const __bf16*>(d_o), w.nl, w.nd, static_cast<__bf16*>(dk),
                      static_cast<__bf16*>(dv));
   if (sa.P > 1)
-    hipLaunchKernelGGL((bwd_split_sum<D, BK, NW>), dim3((unsigned)w.split.n_cols), dim3(64 * NW), 0, stream, p, sv,
+    hipLaunchKernelGGL((bwd_split_sum<D, BK, NW>), dim3((unsigned)w.split.n_cols, C::MD), dim3(64 * NW), 0, stream, p, sv,
                        sa, static_cast<__bf16*>(dk), static_cast<__bf16*>(dv));
   return hipGetLastError();
 }
