@@ -83,6 +83,8 @@ ODD = [
     # the pipelined dQ pass (128-key blocks) at head dimension 64
     ("gqa2_d64_t128", 1, 600, 600, 4, 2, 64, 8, 150, 128, 128, 0, 0),
     ("gqa4_d64_tq64_t128", 1, 700, 700, 8, 2, 64, 8, 150, 64, 128, 0, 0),
+    # a sink of three 128-key blocks, each split into parts in the dK/dV pass
+    ("wide_sink", 1, 1500, 1500, 8, 2, 128, 300, 64, 128, 128, 0, 0),
 ]
 
 

@@ -65,6 +65,8 @@ RAGGED_CASES = [
     ("tuples", [(400, 400), (90, 1200), (1000, 1500)], 8, 4, 128, 0, 0, 64, 128,
      [(16, 128, 0, 300), (16, 128, 300, 300), (0, 64, 600, 900), (100, 0, 0, 50)]),
     ("tp_rank", [(1500, 2000), (2048, 2048)], 4, 1, 128, 32, 256, 128, 128, None),
+    # split sink blocks (three per sequence) with a sequence shorter than three blocks
+    ("wide_sink", [(200, 200), (1500, 1500), (600, 900)], 8, 2, 128, 300, 64, 128, 128, None),
 ]
 
 
