@@ -186,8 +186,10 @@ cowa::HeadGeo geo_of(const cowa_params* p, const Layout& L, int b, int h) {
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 // Split plan of the dK/dV pass (cowa::BwdSplit): the leading KV blocks that hold
-// sink keys of some head are split into P parts, P = ceil(longest such column /
-// longest other column) (at most 16, and at most 256 MB of partials).  A
+// sink keys of some head are split into P parts, P = ceil(2 x longest such
+// column / longest other column) (at most 16, and at most 256 MB of partials):
+// parts of about half an ordinary column, which fill the ends of the other
+// workgroups' queues when the grid is a few rounds of the device.  A
 // column past the sink holds at most the query blocks of its near run
 // (B_k + w_near - 1 distance-0 keys) and of its long-range run
 // (B_k + hi - lo - 1), each spanning up to one block more than its length.
@@ -215,7 +217,7 @@ cowa::BwdSplit bwd_split_plan(const cowa_params* p, const Layout& L) {
     }
   }
   const int64_t seqs = L.ragged ? (int64_t)L.seq.size() : p->batch;
-  int64_t P = std::min<int64_t>((l_sink + l_other - 1) / l_other, 16);
+  int64_t P = std::min<int64_t>((2 * l_sink + l_other - 1) / l_other, 16);
   const size_t col_bytes = cowa::bwd_part_floats(*p) * sizeof(float);
   while (P > 1 && (size_t)(seqs * p->h_k * S * P) * col_bytes > (size_t(256) << 20)) --P;
   if (P <= 1) return sp;

@@ -135,7 +135,8 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
       wi.unit = us % p.h_k;
     }
   } else {
-    wi = cluster_item(blockIdx.x - sa.n_extra, sv.n_kt, 1, grid_units(p, sv), 32, false);
+    wi = cluster_item(blockIdx.x - sa.n_extra, sv.n_kt, 1, grid_units(p, sv),
+                      cluster_rows(sv.n_kt, grid_units(p, sv), 32), false);
   }
   int hk;
   const SeqCtx sc = seq_ctx(p, sv, wi.row, wi.unit, false, hk);
@@ -632,7 +633,8 @@ __global__ void __launch_bounds__(256 * 64 / NQW) bwd_dq_kernel(cowa_params p, S
   const int G = p.h_q / p.h_k;
   // rows of 16 QO blocks x the head groups of one KV head share an XCD's L2;
   // latest (longest) QO blocks first
-  const WorkItem wi = cluster_item(blockIdx.x, sv.n_qt, G / hpw, grid_units(p, sv), 16, true);
+  const WorkItem wi = cluster_item(blockIdx.x, sv.n_qt, G / hpw, grid_units(p, sv),
+                                   cluster_rows(sv.n_qt, grid_units(p, sv), 16), true);
   int hk;
   const SeqCtx sc = seq_ctx(p, sv, wi.row, wi.unit, true, hk);
   const int i = sc.tile;

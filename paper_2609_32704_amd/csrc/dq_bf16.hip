@@ -84,7 +84,8 @@ __global__ void __launch_bounds__(256) bwd_dq32(cowa_params p, SchedView sv, con
   const int G = p.h_q / p.h_k;
   // rows of 16 QO blocks x the head groups of one KV head share an XCD's L2;
   // latest (longest) QO blocks first
-  const WorkItem wi = cluster_item(blockIdx.x, sv.n_qt, G / C::HPW, grid_units(p, sv), 16, true);
+  const WorkItem wi = cluster_item(blockIdx.x, sv.n_qt, G / C::HPW, grid_units(p, sv),
+                                   cluster_rows(sv.n_qt, grid_units(p, sv), 16), true);
   int hk;
   const SeqCtx sc = seq_ctx(p, sv, wi.row, wi.unit, true, hk);
   const int i = sc.tile;

@@ -77,6 +77,18 @@ __device__ inline WorkItem cluster_item(int id, int n_rows, int groups, int unit
   return w;
 }
 
+// Rows per cluster for cluster_item: at most cq_max, halved (down to 4) until
+// there are at least 16 clusters per XCD.  The dispatcher hands workgroup ids to
+// the XCDs round-robin, so each XCD takes a fixed share of the clusters; rows of
+// unequal length (at one end of a sequence only some rows reach a long-range
+// window or the sink) must spread over many clusters to load every XCD alike
+// when there are few units (one KV head on a device, one short sequence).
+__device__ inline int cluster_rows(int n_rows, int units, int cq_max) {
+  int cq = cq_max;
+  while (cq > 4 && (int64_t)units * (n_rows / cq) < 8 * 16) cq >>= 1;
+  return cq;
+}
+
 // XOR applied to the 16-byte chunk index of a row; depends on row % 16 only.
 // The gfx950 LDS has 64 four-byte banks (256 bytes per clock).  Measured with
 // bank-conflict counters: ds_read_b128 serves 16 lanes per clock, in the

@@ -203,11 +203,12 @@ def test_bwd_workspace_holds_sink_column_parts(offset):
     """One rank of an 8-way KV-head split at 131072 tokens: the sink block's
     query list spans all 1024 query blocks, a column past the sink holds at
     most (128 + 4096 - 2) // 128 + 2 = 34 near and (128 + 15856 - 2) // 128 + 2
-    = 126 long-range blocks, so the sink column is cut into ceil(1024 / 160) = 7
-    parts, whose float32 dK/dV partials (2 x 128 x 128 x 4 bytes each) follow
-    the two per-row arrays in the workspace."""
+    = 126 long-range blocks, so the sink column is cut into ceil(2 x 1024 / 160)
+    = 13 parts (about half an ordinary column each), whose float32 dK/dV
+    partials (2 x 128 x 128 x 4 bytes each) follow the two per-row arrays in
+    the workspace."""
     p = cowa.make_params(1, 131072, 131072, 4, 1, 128, 128, 4096, 128, 128, h_k_total=8, h_k_offset=offset)
-    assert abi.cowa_bwd_workspace_size(p) == _split_ws(4 * 131072, 1, 7, 128, 128)
+    assert abi.cowa_bwd_workspace_size(p) == _split_ws(4 * 131072, 1, 13, 128, 128)
 
 
 def test_bwd_workspace_without_sink_has_no_parts():
@@ -215,10 +216,10 @@ def test_bwd_workspace_without_sink_has_no_parts():
     p = cowa.make_params(1, 8192, 8192, 32, 8, 128, 0, 8192, 64, 64)
     assert abi.cowa_bwd_workspace_size(p) == _split_ws(32 * 8192, 0, 1, 64, 128)
     # the 8K workload (64-token blocks): sink column of 128 blocks, others at
-    # most (64 + 1024 - 2) // 64 + 2 + (64 + 888 - 2) // 64 + 2 = 34 -> 4 parts,
-    # for each of the 8 KV heads
+    # most (64 + 1024 - 2) // 64 + 2 + (64 + 888 - 2) // 64 + 2 = 34 -> ceil(256 / 34)
+    # = 8 parts, for each of the 8 KV heads
     p = cowa.make_params(1, 8192, 8192, 32, 8, 128, 64, 1024, 64, 64)
-    assert abi.cowa_bwd_workspace_size(p) == _split_ws(32 * 8192, 8, 4, 64, 128)
+    assert abi.cowa_bwd_workspace_size(p) == _split_ws(32 * 8192, 8, 8, 64, 128)
 
 
 def test_decode_argument_errors_on_host():
