@@ -444,6 +444,25 @@ def main():
                 workloads[f"tp8_rank{r}"] = dict(
                     time_train(par, q[:, :4], k[:, :1], v[:, :1], do[:, :4], 5),
                     shape=f"131072 tokens, one rank of 8: global KV head {r}, 4 QO heads")
+            # the forward with a wide score range: Q scaled by 40, so that in most rows a later
+            # score exceeds the exponent offset fixed from the row's first 32 keys by more than
+            # 2^64 and the row runs a second pass (the worst case of the fixed-offset softmax)
+            qw = (q.float() * 40.0).to(torch.bfloat16)
+            ow = torch.empty_like(qw)
+            tw = 0.0
+            for it in range(4):
+                e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+                e[0].record()
+                _abi.cowa_fwd(p, sched.s, qw.data_ptr(), k.data_ptr(), v.data_ptr(), ow.data_ptr(), lse.data_ptr(),
+                              stream)
+                e[1].record()
+                torch.cuda.synchronize()
+                if it:
+                    tw += e[0].elapsed_time(e[1]) / 3
+            workloads["fwd_wide_scores"] = {
+                "fwd_ms": tw, "fwd_ms_normal_scores": per["fwd"], "slowdown": tw / per["fwd"],
+                "shape": "the 131072-token forward with Q scaled by 40 (most rows run the second pass)"}
+            del qw, ow
 
     dense = None
     if not args.no_dense and args.dense_iters > 0:

@@ -68,7 +68,9 @@ struct Dq32Cfg {
   static constexpr int MAIN_BYTES = 4 * T::BYTES;  // K and V of two blocks; then the row's entry lists
   static constexpr int LDS_MAX = 160 * 1024;
   static int lds_bytes(int n_kt) { return MAIN_BYTES + 4 * n_kt; }
+  static constexpr int OUT_PITCH = 2 * D + 16;  // staged dQ rows (bytes), in the K/V buffers at the end
   static_assert(KS == 2 * MD, "one dQ^T product group per k-step slot");
+  static_assert(4 * NQW * OUT_PITCH <= MAIN_BYTES, "staged rows fit the K/V buffers");
 };
 
 template <int D, int BQ>
@@ -101,9 +103,33 @@ __global__ void __launch_bounds__(256) bwd_dq32(cowa_params p, SchedView sv, con
   const __bf16* vbase = v + (sc.k0 + (int64_t)hk * sc.kh) * D;
   const uint32_t smem_base = lds_addr(smem);
 
-  // zero the K/V buffers once: key rows past the end of the sequence are not
-  // copied (the buffer loads return zero there) and must hold finite values
-  for (int x = tid; x < C::MAIN_BYTES / 16; x += blockDim.x) reinterpret_cast<u32x4*>(smem)[x] = u32x4{0u, 0u, 0u, 0u};
+  // Q^T and dO^T fragments (B operands): query column 32 nq + l32, d = 16 ks + 8 hh + 0..7;
+  // the row values of that query: the exponent offset -LSE log2 e (-inf for a
+  // row past n_q or without keys, so P = 0 there) and -D.  Loaded first, so
+  // that their latency overlaps that of the entry lists.
+  const int64_t row_base = sc.q0 + (int64_t)hq * sc.qh;
+  bf16x8 qf[NQT][KS], gf[NQT][KS];
+  float mlse[NQT], dn[NQT];
+#pragma unroll
+  for (int nq = 0; nq < NQT; ++nq) {
+    const int qp = q_first + nq * 32 + l32;
+    const bool ok = qp < n_q;
+    const int64_t row = row_base + (ok ? qp : 0);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(q + row * D + ks * 16 + 8 * hh);
+      const bf16x8 b = *reinterpret_cast<const bf16x8*>(d_o + row * D + ks * 16 + 8 * hh);
+      qf[nq][ks] = ok ? a : bf16x8{};
+      gf[nq][ks] = ok ? b : bf16x8{};
+    }
+    const float nlv = ok ? nl[row] : -INFINITY;
+    mlse[nq] = nlv == INFINITY ? -INFINITY : nlv;
+    dn[nq] = ok ? nd[row] : 0.f;
+  }
+  // zero the K/V buffers once when the last KV block is partial: key rows past
+  // the end of the sequence are not copied and must hold finite values
+  if (n_k % BK != 0)
+    for (int x = tid; x < C::MAIN_BYTES / 16; x += blockDim.x) reinterpret_cast<u32x4*>(smem)[x] = u32x4{0u, 0u, 0u, 0u};
 
   // the row's entries, split into full (from the front) and partial (from the back) lists
   const int r = sc.sched;
@@ -159,28 +185,6 @@ __global__ void __launch_bounds__(256) bwd_dq32(cowa_params p, SchedView sv, con
   };
   __syncthreads();  // the lists and the zeroed buffers are in LDS
 
-  // Q^T and dO^T fragments (B operands): query column 32 nq + l32, d = 16 ks + 8 hh + 0..7;
-  // the row values of that query: the exponent offset -LSE log2 e (-inf for a
-  // row past n_q or without keys, so P = 0 there) and -D
-  const int64_t row_base = sc.q0 + (int64_t)hq * sc.qh;
-  bf16x8 qf[NQT][KS], gf[NQT][KS];
-  float mlse[NQT], dn[NQT];
-#pragma unroll
-  for (int nq = 0; nq < NQT; ++nq) {
-    const int qp = q_first + nq * 32 + l32;
-    const bool ok = qp < n_q;
-    const int64_t row = row_base + (ok ? qp : 0);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(q + row * D + ks * 16 + 8 * hh);
-      const bf16x8 b = *reinterpret_cast<const bf16x8*>(d_o + row * D + ks * 16 + 8 * hh);
-      qf[nq][ks] = ok ? a : bf16x8{};
-      gf[nq][ks] = ok ? b : bf16x8{};
-    }
-    const float nlv = ok ? nl[row] : -INFINITY;
-    mlse[nq] = nlv == INFINITY ? -INFINITY : nlv;
-    dn[nq] = ok ? nd[row] : 0.f;
-  }
   // dQ^T accumulators: element (lane, e) is d = 32 md + 8 (e / 4) + 4 hh + e % 4, query 32 nq + l32
   f32x16 qacc[MD][NQT];
 #pragma unroll
@@ -416,13 +420,16 @@ __global__ void __launch_bounds__(256) bwd_dq32(cowa_params p, SchedView sv, con
     if (n_ent > 0) drain(n_ent - 1);
   }
 
-  // dQ = scale dQ^T, written once per row
+  // dQ = scale dQ^T, written once per row through LDS: once every wave's last
+  // reads are done, each wave stages its 64 rows and stores whole rows, 16
+  // bytes per lane, instead of 16-byte pieces of 32 rows per store in the
+  // accumulator layout
   const float scale = p.softmax_scale;
+  constexpr int OP = C::OUT_PITCH;
+  unsigned char* ot = smem + wave * C::NQW * OP;
+  __syncthreads();
 #pragma unroll
-  for (int nq = 0; nq < NQT; ++nq) {
-    const int qp = q_first + nq * 32 + l32;
-    if (qp >= n_q) continue;
-    __bf16* drow = dq + (row_base + qp) * D;
+  for (int nq = 0; nq < NQT; ++nq)
 #pragma unroll
     for (int md = 0; md < MD; ++md)
 #pragma unroll
@@ -430,8 +437,15 @@ __global__ void __launch_bounds__(256) bwd_dq32(cowa_params p, SchedView sv, con
         bf16x4 ov;
 #pragma unroll
         for (int rr = 0; rr < 4; ++rr) ov[rr] = (__bf16)(scale * qacc[md][nq][4 * j4 + rr]);
-        *reinterpret_cast<bf16x4*>(drow + md * 32 + 8 * j4 + 4 * hh) = ov;
+        *reinterpret_cast<bf16x4*>(ot + (nq * 32 + l32) * OP + (md * 32 + 8 * j4 + 4 * hh) * 2) = ov;
       }
+  constexpr int CPR = D / 8;  // 16-byte chunks per row
+#pragma unroll
+  for (int x = 0; x < C::NQW * CPR / 64; ++x) {
+    const int c = x * 64 + lane, row = c / CPR, ch = c % CPR;
+    if (q_first + row < n_q)
+      *reinterpret_cast<u32x4*>(dq + (row_base + q_first + row) * D + ch * 8) =
+          *reinterpret_cast<const u32x4*>(ot + row * OP + ch * 16);
   }
 }
 

@@ -89,7 +89,11 @@ struct FwdCfg {
   using T = SwzTile<D, BK>;
   static constexpr int MAIN_BYTES = 4 * T::BYTES;  // K and V of two blocks; then the row's entry lists
   static constexpr int LDS_MAX = 160 * 1024;
-  static int lds_bytes(int n_kt) { return MAIN_BYTES + 4 * n_kt + 16; }  // + a vote word
+  static constexpr int OUT_PITCH = 2 * D + 16;               // staged output rows (bytes)
+  static constexpr int OUT_BYTES = NWF * NQW * OUT_PITCH;    // reuses the K/V buffers and lists at the end
+  static int lds_bytes(int n_kt) {                           // + a vote word
+    return MAIN_BYTES + 4 * n_kt + 16 > OUT_BYTES ? MAIN_BYTES + 4 * n_kt + 16 : OUT_BYTES;
+  }
   static int max_kblocks() { return (LDS_MAX - MAIN_BYTES - 16) / 4; }
   static_assert(KS == 2 * MD, "S and O groups alternate one to one");
   static_assert(NCH == 2 || NCH == 4, "64- or 128-key blocks");
@@ -129,9 +133,25 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   const __bf16* vbase = v + (sc.k0 + (int64_t)hk * sc.kh) * D;
   const uint32_t smem_base = lds_addr(smem);
 
-  // zero the K/V buffers once: key rows past the end of the sequence are not
-  // copied (the buffer loads return zero there) and must hold finite values
-  for (int x = tid; x < C::MAIN_BYTES / 16; x += blockDim.x) reinterpret_cast<u32x4*>(smem)[x] = u32x4{0u, 0u, 0u, 0u};
+  // Q^T fragments (B operands): query column 32 nq + l32, d = 16 ks + 8 hh + 0..7;
+  // loaded first, so that their latency overlaps that of the entry lists
+  const int64_t row_base = sc.q0 + (int64_t)hq * sc.qh;
+  bf16x8 qf[NQT][KS];
+#pragma unroll
+  for (int nq = 0; nq < NQT; ++nq) {
+    const int qp = q_first + nq * 32 + l32;
+    const bool ok = qp < n_q;
+    const __bf16* qrow = q + (row_base + (ok ? qp : 0)) * D;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 val = *reinterpret_cast<const bf16x8*>(qrow + ks * 16 + 8 * hh);
+      qf[nq][ks] = ok ? val : bf16x8{};
+    }
+  }
+  // zero the K/V buffers once when the last KV block is partial: key rows past
+  // the end of the sequence are not copied and must hold finite values
+  if (n_k % BK != 0)
+    for (int x = tid; x < C::MAIN_BYTES / 16; x += blockDim.x) reinterpret_cast<u32x4*>(smem)[x] = u32x4{0u, 0u, 0u, 0u};
 
   // the row's entries, split into full (from the front) and partial (from the back) lists
   const int r = sc.sched;
@@ -194,20 +214,6 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   };
   __syncthreads();  // the lists and the zeroed buffers are in LDS
 
-  // Q^T fragments (B operands): query column 32 nq + l32, d = 16 ks + 8 hh + 0..7
-  const int64_t row_base = sc.q0 + (int64_t)hq * sc.qh;
-  bf16x8 qf[NQT][KS];
-#pragma unroll
-  for (int nq = 0; nq < NQT; ++nq) {
-    const int qp = q_first + nq * 32 + l32;
-    const bool ok = qp < n_q;
-    const __bf16* qrow = q + (row_base + (ok ? qp : 0)) * D;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const bf16x8 val = *reinterpret_cast<const bf16x8*>(qrow + ks * 16 + 8 * hh);
-      qf[nq][ks] = ok ? val : bf16x8{};
-    }
-  }
   // LDS fragment offsets for chunk 0 of a tile (the swizzle depends on row % 16,
   // so chunks 32 rows further and k-steps 16 rows further add plain row bytes)
   //  K (A operand of S^T): row l32, columns 16 ks + 8 hh + 0..7;
@@ -519,14 +525,18 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
     if (!again) break;
   }
 
-  // O = O / l; LSE = (m + log2 l) ln 2 with the offset m of the last pass (base 2)
+  // O = O / l; LSE = (m + log2 l) ln 2 with the offset m of the last pass (base 2).
+  // O goes out through LDS (free here: every wave is past the vote's barriers,
+  // its reads are done and its copies have landed): each wave stages its 64
+  // rows and stores whole rows, 16 bytes per lane, instead of 16-byte pieces of
+  // 32 rows per store in the accumulator layout.
+  constexpr int OP = C::OUT_PITCH;
+  unsigned char* ot = smem + wave * C::NQW * OP;
 #pragma unroll
   for (int nq = 0; nq < NQT; ++nq) {
     const float lt = l_run[nq] + __shfl_xor(l_run[nq], 32);
     const int qp = q_first + nq * 32 + l32;
-    if (qp >= n_q) continue;
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
-    __bf16* orow = o + (row_base + qp) * D;
 #pragma unroll
     for (int md = 0; md < MD; ++md)
 #pragma unroll
@@ -534,9 +544,17 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
         bf16x4 ov;
 #pragma unroll
         for (int rr = 0; rr < 4; ++rr) ov[rr] = (__bf16)(oacc[md][nq][4 * j4 + rr] * inv);
-        *reinterpret_cast<bf16x4*>(orow + md * 32 + 8 * j4 + 4 * hh) = ov;
+        *reinterpret_cast<bf16x4*>(ot + (nq * 32 + l32) * OP + (md * 32 + 8 * j4 + 4 * hh) * 2) = ov;
       }
-    if (hh == 0) lse[row_base + qp] = lt > 0.f ? (mu[nq] + __log2f(lt)) * kLn2 : -INFINITY;
+    if (hh == 0 && qp < n_q) lse[row_base + qp] = lt > 0.f ? (mu[nq] + __log2f(lt)) * kLn2 : -INFINITY;
+  }
+  constexpr int CPR = D / 8;  // 16-byte chunks per row
+#pragma unroll
+  for (int x = 0; x < C::NQW * CPR / 64; ++x) {
+    const int c = x * 64 + lane, row = c / CPR, ch = c % CPR;
+    if (q_first + row < n_q)
+      *reinterpret_cast<u32x4*>(o + (row_base + q_first + row) * D + ch * 8) =
+          *reinterpret_cast<const u32x4*>(ot + row * OP + ch * 16);
   }
 }
 
