@@ -243,14 +243,20 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   f32x16 sacc[2][NQT];
   u32x4 pbw[2][2][NQT];  // P^T of two chunks: bf16 pairs, [chunk % 2][k-step][query tile]
 
-  // The exponent offset m (base 2, per query column) is fixed once per row:
-  // the maximum over the first 32 keys of the row's first block.  P = exp2(s c - m)
-  // may exceed 1; O and l share the offset, so O / l and LSE = (m + log2 l) ln 2
-  // are unaffected and O never needs rescaling.  If a later score exceeds m by
-  // more than kLimit (P > 2^kLimit, where bf16 P and fp32 sums would approach
-  // their range), or m was unset, the workgroup runs the row again with m set
-  // to the row maximum found by the first pass.
-  constexpr float kLimit = 64.f;
+  // The exponent offset m (base 2, per query column) starts kHead above the
+  // maximum over the first 32 keys of the row's first block, so P = exp2(s c - m)
+  // is at most 2^-kHead there and a later score may pass that maximum by
+  // kHead + ~110 before P, l or O could overflow (keys more than ~60 below the
+  // maximum underflow, 2^-60 of the largest term).  O and l share the offset,
+  // so O / l and LSE = (m + log2 l) ln 2 are unaffected, and O is rescaled
+  // only when, at the end of a block, a column's maximum has passed the one
+  // that m was set from by more than kLimit: then m moves to kHead above it
+  // and O, l and the P^T not yet in O are multiplied by 2^(m_old - m) once
+  // (rare after the first blocks of a row, never for scores within kLimit).
+  // If P, l or O overflowed anyway, the workgroup runs the row again with m
+  // set from the row maximum found by the first pass, as it does when m was
+  // unset (no legal key among the first 32) but the row has legal keys.
+  constexpr float kHead = 64.f, kLimit = 32.f;
   float m_fix[NQT], m_hi[NQT], l_run[NQT], mu[NQT];  // m_hi: this lane's maximum raw score per column
 #pragma unroll
   for (int nq = 0; nq < NQT; ++nq) m_fix[nq] = -INFINITY;
@@ -311,6 +317,54 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   // back; with 128-key blocks, V of block t is needed from its third step on,
   // so it is copied in the middle of block t - 1, once V of block t - 2 is no
   // longer read.
+  // End of a block: move the offset of columns whose maximum has passed it by
+  // more than kLimit.  P^T of the block's second-to-last chunk is computed but
+  // not yet in O (it enters in the next block's first chunk step), so it is
+  // rescaled with O and l; the last chunk is exponentiated after this point.
+  // The test is per lane (a column's two lanes hold disjoint keys, and the one
+  // holding the maximum sees it); the new offset is kHead above the column
+  // maximum.  `hot` records a P above 2^kHot, the only way P, l or O can
+  // approach the float range, so the overflow check at the end of a pass runs
+  // only then.
+  constexpr float kHot = 64.f;
+  bool hot = false;
+  auto rebase = [&]() __attribute__((always_inline)) {
+    bool need = false;
+#pragma unroll
+    for (int nq = 0; nq < NQT; ++nq) {
+      const float e = m_hi[nq] * c - mu[nq];
+      need |= e > kLimit - kHead;
+      hot |= e > kHot;
+    }
+    if (__ballot(need) == 0) return;
+    constexpr int PS = (NCH - 2) & 1;  // pair buffer of the pending chunk
+#pragma unroll
+    for (int nq = 0; nq < NQT; ++nq) {
+      const float mh = fmaxf(m_hi[nq], __shfl_xor(m_hi[nq], 32)) * c + kHead;
+      const bool mv = mh > mu[nq] + kLimit;
+      const float f = mv ? __builtin_amdgcn_exp2f(mu[nq] - mh) : 1.f;
+      mu[nq] = mv ? mh : mu[nq];
+      l_run[nq] *= f;
+#pragma unroll
+      for (int md = 0; md < MD; ++md) {  // one tile at a time, back into its AGPRs
+#pragma unroll
+        for (int x = 0; x < 16; ++x) oacc[md][nq][x] *= f;
+        asm volatile("" : "+a"(oacc[md][nq]));
+      }
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          // (a vector element is copied out first: bit-casting the element
+          // expression itself reads element 0)
+          const uint32_t u = pbw[PS][kk][nq][w];
+          const bf16x2 pk = __builtin_bit_cast(bf16x2, u);
+          const bf16x2 sc2 = {(__bf16)((float)pk[0] * f), (__bf16)((float)pk[1] * f)};
+          pbw[PS][kk][nq][w] = __builtin_bit_cast(uint32_t, sc2);
+        }
+    }
+  };
+
   constexpr int PF = 2, RING = PF + 2;
   int k_prev = 0;  // first key of the previous block
   // One block.  FIRST: the row's first block (nothing before its first chunk).
@@ -410,6 +464,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
     // anything reads them
     mfma_settle(sacc[1]);
     __builtin_amdgcn_sched_barrier(0);
+    rebase();
     // register placement: O^T accumulators and Q^T fragments in AGPRs (read
     // directly by the matrix cores), S^T and P^T in VGPRs; these emit nothing
 #pragma unroll
@@ -504,17 +559,31 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
       }
     }
 #pragma unroll
-    for (int nq = 0; nq < NQT; ++nq) mu[nq] = m_fix[nq] == -INFINITY ? 0.f : m_fix[nq];
+    for (int nq = 0; nq < NQT; ++nq) mu[nq] = m_fix[nq] == -INFINITY ? 0.f : m_fix[nq] + kHead;
     sweep();
-    // did a score exceed its column's offset by more than kLimit?
+    // was a column's offset unset although it met legal keys later, or did P,
+    // l or O overflow (possible only after a P above 2^kHot)?
     bool far = false;
 #pragma unroll
     for (int nq = 0; nq < NQT; ++nq) {
+      hot |= m_hi[nq] * c - mu[nq] > kHot;  // (the last chunk came after the last block end)
       const float mh = fmaxf(m_hi[nq], __shfl_xor(m_hi[nq], 32)) * c;  // the column maximum, exponent units
-      // (a column whose offset is unset but which met legal keys later is run again too)
-      far |= mh != -INFINITY && (m_fix[nq] == -INFINITY || mh > m_fix[nq] + kLimit);
-      m_fix[nq] = mh;  // the offset of a second pass: then P <= 1 everywhere
+      far |= mh != -INFINITY && m_fix[nq] == -INFINITY;
+      m_fix[nq] = mh;  // the offset of a second pass: then P <= 2^-kHead everywhere
     }
+    if (__ballot(hot) != 0) {
+#pragma unroll
+      for (int nq = 0; nq < NQT; ++nq) {
+        far |= !__builtin_isfinite(l_run[nq]);
+#pragma unroll
+        for (int md = 0; md < MD; ++md) {
+#pragma unroll
+          for (int x = 0; x < 16; ++x) far |= !__builtin_isfinite(oacc[md][nq][x]);
+          asm volatile("" : "+a"(oacc[md][nq]));
+        }
+      }
+    }
+    hot = false;
     // workgroup vote through a word past the block lists
     if (tid == 0) *vote = 0;
     __syncthreads();

@@ -82,18 +82,21 @@ def test_fwd_deterministic():
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
 
 
-def test_fwd_wide_score_range():
-    """Keys of the second 128-key block score far above the rest (about 90 in
-    log2 units), so rows whose first processed block is another one exceed the
-    forward's fixed exponent offset by more than its limit and run a second
-    pass with the row maximum; the fp64 oracle has no such limit."""
+@pytest.mark.parametrize("lift,lse_min", [(4.0, 60.0), (9.0, 130.0)])
+def test_fwd_wide_score_range(lift, lse_min):
+    """Keys of the second 128-key block score far above the rest, so rows whose
+    first processed block is another one pass the forward's starting exponent
+    offset by a wide margin.  lift 4 (about 90 in log2 units): the offset moves
+    at the end of that block and O, l and the pending P are rescaled once.
+    lift 9 (about 200): P overflows within the block, and the row runs its
+    second pass with the row maximum.  The fp64 oracle has no offset at all."""
     dev = need_gpu()
     import paper_2609_32704_amd as cowa
     n, h_q, h_k, d = 512, 2, 1, 64
     rng = np.random.default_rng(11)
     qf = (rng.standard_normal((1, h_q, n, d)) * 0.25 + 2.0).astype(np.float32)
     kf = (rng.standard_normal((1, h_k, n, d)) * 0.1).astype(np.float32)
-    kf[:, :, 128:256, :] += 4.0
+    kf[:, :, 128:256, :] += lift
     vf = rng.standard_normal((1, h_k, n, d)).astype(np.float32)
     bits = [inputs.f32_to_bf16_bits(x) for x in (qf, kf, vf)]
     vals = [inputs.bf16_bits_to_f64(b) for b in bits]
@@ -104,6 +107,6 @@ def test_fwd_wide_score_range():
     cowa.fwd(q, k, v, 16, 512, 128, 128, scale, out=o, lse=lse)
     torch.cuda.synchronize()
     o_r, l_r = ref.forward(vals[0], vals[1], vals[2], 16, 512, scale)
-    assert l_r.max() > 60.0  # the range that needs the second pass
+    assert l_r.max() > lse_min  # the score range of the case
     compare("O", to_host(o), o_r)
     compare("LSE", to_host(lse), l_r)
