@@ -42,6 +42,7 @@ import argparse
 import hashlib
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -325,11 +326,8 @@ def main():
         step(evs)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    per = {n: 0.0 for n in names}
-    for evs in all_evs:
-        for idx, n in enumerate(names):
-            per[n] += evs[idx].elapsed_time(evs[idx + 1])
-    per = {n: per[n] / args.steps for n in names}
+    samples = {n: [evs[idx].elapsed_time(evs[idx + 1]) for evs in all_evs] for idx, n in enumerate(names)}
+    per = {n: sum(x) / args.steps for n, x in samples.items()}
     if args.only != "all":
         log("per-kernel ms:", {n: round(x, 3) for n, x in per.items()})
         return
@@ -357,11 +355,23 @@ def main():
         "decode": {"ms": per["decode"], "bound": "hbm", "unit": "GB/s", "work": dec_bytes,
                    "achieved": dec_bytes / (per["decode"] * 1e-3) / 1e9},
     }
-    for kn in kernels.values():
+    for n, kn in kernels.items():
+        kn["ms_median"] = statistics.median(samples[n])
+        kn["ms_min"] = min(samples[n])
         if kn["bound"] == "mfma":
             kn["frac"] = kn["achieved"] / PEAK_BF16_TFLOPS
         elif kn["bound"] == "hbm":
             kn["frac"] = kn["achieved"] / PEAK_HBM_GBPS
+    # tile-FLOP rates: every listed tile (schedule entry x QO heads of its group x
+    # sequences) at its full B_q x B_k size, i.e. the work the matrix cores see
+    # including the masked part of partial tiles
+    tile_pairs = sched.nnz * (T["h_q"] // T["h_k"]) * T["batch"] * T["tile"] * T["tile"]
+    for n, per_pair in (("fwd", 4), ("bwd_main", 8), ("bwd_dq", 6)):
+        kernels[n]["tile_tflops"] = per_pair * T["d"] * tile_pairs / (per[n] * 1e-3) / 1e12
+    kernels["fwd"]["tile_fill"] = pairs / tile_pairs
+    # the split partials (m, l and float32 O per split and QO head): written by
+    # the split kernel, read by the combine kernel; not in the algorithmic bytes
+    kernels["decode"]["partial_state_bytes"] = 2 * dws.numel()
 
     if ceil:
         for kn in kernels.values():
