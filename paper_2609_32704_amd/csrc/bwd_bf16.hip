@@ -252,7 +252,8 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
     hh = hh < G ? hh : G - 1;
     const int q0 = (int)(ent >> 1) * p.tile_q + sub * C::BQ;
     const int64_t row_base = sc.q0 + (int64_t)(hk * G + hh) * sc.qh;
-    const uint32_t bytes = (uint32_t)(n_q - q0) * D * 2;
+    // a sub-block wholly past n_q (the last QO block's second half) reads nothing
+    const uint32_t bytes = q0 < n_q ? (uint32_t)(n_q - q0) * D * 2 : 0u;
     const int r = q0 + lane;
     const int rc = r < n_q ? r : n_q - 1;
     return StageSrc{(row_base + q0) * D * 2, bytes, ((wave & 1) ? nd : nl) + row_base + rc};

@@ -134,3 +134,37 @@ def test_bwd_bitwise_deterministic_8k():
     second = _run_bwd(w, t, dev)
     for a, b, n in zip(first, second, ("dQ", "dK", "dV")):
         assert torch.equal(a, b), f"{n} differs between two identical runs"
+
+
+def test_bwd_reads_no_rows_past_the_sequence():
+    """Regression: with 128-row QO blocks and n_q % 128 <= 64, the last block's
+    second 64-row step lies wholly past n_q.  Its copies of Q and dO must read
+    nothing (they once read past the end of the tensors).  Q and dO sit at the
+    start of NaN-filled buffers here, so a row read past the last QO head's end
+    would turn dK and dV into NaN; the reads stay inside those buffers."""
+    import paper_2609_32704_amd as cowa
+    dev = need_gpu()
+    n, h_q, h_k, d, sink, near, tile = 3000, 4, 2, 128, 16, 256, 128
+    assert 0 < n % tile <= 64
+    t = {nm: inputs.normal_bf16(s, inputs.seed_sequence(inputs.key_of("past_end", n), nm))
+         for nm, s in (("q", (1, h_q, n, d)), ("k", (1, h_k, n, d)), ("v", (1, h_k, n, d)), ("do", (1, h_q, n, d)))}
+    k, v = to_dev(t["k"][0], dev), to_dev(t["v"][0], dev)
+
+    def padded(bits):  # the tensor at the start of a buffer with 256 NaN rows behind it
+        buf = torch.full(((h_q * n + 256) * d,), float("nan"), dtype=torch.bfloat16, device=dev)
+        view = buf[:h_q * n * d].view(1, h_q, n, d)
+        view.copy_(to_dev(bits, dev))
+        return buf, view
+
+    qbuf, q = padded(t["q"][0])
+    dobuf, do = padded(t["do"][0])
+    scale = d ** -0.5
+    o, lse = cowa.fwd(q, k, v, sink, near, tile, tile, scale)
+    dq, dk, dv = (torch.full_like(x, float("nan")) for x in (q, k, v))
+    cowa.bwd(q, k, v, o, lse, do, sink, near, tile, tile, scale, dq=dq, dk=dk, dv=dv)
+    torch.cuda.synchronize()
+    dq_r, dk_r, dv_r, _, _ = ref.backward(t["q"][1], t["k"][1], t["v"][1], t["do"][1], sink, near, scale)
+    compare("dQ", to_host(dq), dq_r)
+    compare("dK", to_host(dk), dk_r)
+    compare("dV", to_host(dv), dv_r)
+    del qbuf, dobuf
