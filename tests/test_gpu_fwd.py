@@ -82,17 +82,20 @@ def test_fwd_deterministic():
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
 
 
-@pytest.mark.parametrize("lift,lse_min", [(4.0, 60.0), (9.0, 130.0)])
-def test_fwd_wide_score_range(lift, lse_min):
+@pytest.mark.parametrize("lift,lse_min,d,tile", [(4.0, 60.0, 64, 128), (9.0, 130.0, 64, 128), (4.0, 60.0, 64, 64),
+                                                 (9.0, 130.0, 64, 64), (3.0, 60.0, 128, 64), (3.0, 60.0, 128, 128)])
+def test_fwd_wide_score_range(lift, lse_min, d, tile):
     """Keys of the second 128-key block score far above the rest, so rows whose
     first processed block is another one pass the forward's starting exponent
     offset by a wide margin.  lift 4 (about 90 in log2 units): the offset moves
     at the end of that block and O, l and the pending P are rescaled once.
     lift 9 (about 200): P overflows within the block, and the row runs its
-    second pass with the row maximum.  The fp64 oracle has no offset at all."""
+    second pass with the row maximum.  With 64-key blocks the pending P^T at a
+    block end is the block's first chunk instead of its third.  The fp64 oracle
+    has no offset at all."""
     dev = need_gpu()
     import paper_2609_32704_amd as cowa
-    n, h_q, h_k, d = 512, 2, 1, 64
+    n, h_q, h_k = 512, 2, 1
     rng = np.random.default_rng(11)
     qf = (rng.standard_normal((1, h_q, n, d)) * 0.25 + 2.0).astype(np.float32)
     kf = (rng.standard_normal((1, h_k, n, d)) * 0.1).astype(np.float32)
@@ -104,7 +107,7 @@ def test_fwd_wide_score_range(lift, lse_min):
     scale = d ** -0.5
     o = torch.full_like(q, float("nan"))
     lse = torch.full((1, h_q, n), float("nan"), dtype=torch.float32, device=dev)
-    cowa.fwd(q, k, v, 16, 512, 128, 128, scale, out=o, lse=lse)
+    cowa.fwd(q, k, v, 16, 512, tile, tile, scale, out=o, lse=lse)
     torch.cuda.synchronize()
     o_r, l_r = ref.forward(vals[0], vals[1], vals[2], 16, 512, scale)
     assert l_r.max() > lse_min  # the score range of the case
