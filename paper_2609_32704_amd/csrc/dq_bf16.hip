@@ -442,7 +442,7 @@ __global__ void __launch_bounds__(256) bwd_dq32(cowa_params p, SchedView sv, con
   constexpr int CPR = D / 8;  // 16-byte chunks per row
 #pragma unroll
   for (int x = 0; x < C::NQW * CPR / 64; ++x) {
-    const int c = x * 64 + lane, row = c / CPR, ch = c % CPR;
+    const int idx = x * 64 + lane, row = idx / CPR, ch = idx % CPR;
     if (q_first + row < n_q)
       *reinterpret_cast<u32x4*>(dq + (row_base + q_first + row) * D + ch * 8) =
           *reinterpret_cast<const u32x4*>(ot + row * OP + ch * 16);

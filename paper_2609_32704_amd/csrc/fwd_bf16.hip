@@ -305,18 +305,6 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
     });
   };
 
-  // Software pipeline over the row's 32-key chunks: chunk n has its S^T
-  // computed in chunk step n, is exponentiated in step n + 1 and enters
-  // O^T += V^T P^T in step n + 2.  Within a chunk step the matrix cores work on
-  // S^T (chunk n) and O^T (chunk n - 2) while the vector ALUs turn S^T of chunk
-  // n - 1 into P^T: the streams are independent, so the exponentials hide under
-  // the products.  Fragments are read PF groups ahead.
-  //
-  // LDS: K of block t in K buffer t % 2, V of block t in V buffer t % 2.  The
-  // O^T products of block t's steps read V of block t - 1 for the chunks two
-  // back; with 128-key blocks, V of block t is needed from its third step on,
-  // so it is copied in the middle of block t - 1, once V of block t - 2 is no
-  // longer read.
   // End of a block: move the offset of columns whose maximum has passed it by
   // more than kLimit.  P^T of the block's second-to-last chunk is computed but
   // not yet in O (it enters in the next block's first chunk step), so it is
@@ -365,6 +353,18 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
     }
   };
 
+  // Software pipeline over the row's 32-key chunks: chunk n has its S^T
+  // computed in chunk step n, is exponentiated in step n + 1 and enters
+  // O^T += V^T P^T in step n + 2.  Within a chunk step the matrix cores work on
+  // S^T (chunk n) and O^T (chunk n - 2) while the vector ALUs turn S^T of chunk
+  // n - 1 into P^T: the streams are independent, so the exponentials hide under
+  // the products.  Fragments are read PF groups ahead.
+  //
+  // LDS: K of block t in K buffer t % 2, V of block t in V buffer t % 2.  The
+  // O^T products of block t's steps read V of block t - 1 for the chunks two
+  // back; with 128-key blocks, V of block t is needed from its third step on,
+  // so it is copied in the middle of block t - 1, once V of block t - 2 is no
+  // longer read.
   constexpr int PF = 2, RING = PF + 2;
   int k_prev = 0;  // first key of the previous block
   // One block.  FIRST: the row's first block (nothing before its first chunk).
@@ -620,7 +620,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   constexpr int CPR = D / 8;  // 16-byte chunks per row
 #pragma unroll
   for (int x = 0; x < C::NQW * CPR / 64; ++x) {
-    const int c = x * 64 + lane, row = c / CPR, ch = c % CPR;
+    const int idx = x * 64 + lane, row = idx / CPR, ch = idx % CPR;
     if (q_first + row < n_q)
       *reinterpret_cast<u32x4*>(o + (row_base + q_first + row) * D + ch * 8) =
           *reinterpret_cast<const u32x4*>(ot + row * OP + ch * 16);
