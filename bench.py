@@ -64,8 +64,19 @@ def log(*a):
 
 
 def source_digest(path):
+    """What a kernel's code object depends on: its source, its per-file compile
+    options and the shared headers of the sources' directory."""
+    from paper_2609_32704_amd.build import FILE_FLAGS
+    h = hashlib.sha256()
     with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+        h.update(f.read())
+    h.update(b"\0" + " ".join(FILE_FLAGS.get(os.path.basename(path), [])).encode())
+    folder = os.path.dirname(path)
+    for name in sorted(os.listdir(folder)):
+        if name.endswith(".h"):
+            with open(os.path.join(folder, name), "rb") as f:
+                h.update(b"\0" + name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
 
 
 def read_traffic(kernel):
