@@ -368,14 +368,24 @@ __global__ void __launch_bounds__(64 * NW) bwd_main(cowa_params p, SchedView sv,
   constexpr int EPC = 8 * C::NTK / NG;
   // (the row values are nl = -LSE log2(e), so x = S c + nl = (S - LSE) log2(e);
   // pacc already holds dP - D)
+  // In a partial block the window rule comes as a bit mask over the half's 32
+  // query rows per key (once per half and key tile, shifted to the lane's rows
+  // 4 lg + 16 i + r); an illegal pair's exponent becomes -inf by a bit select.
+  uint32_t qmask[C::NTK];
   auto soft_chunk = [&](int hf, int ci, const float4 (&l4)[2], bool masked, int q0) {
+    if (masked && ci == 0)
+#pragma unroll
+      for (int nt = 0; nt < C::NTK; ++nt) qmask[nt] = legal_queries32(g, q0 + 32 * hf, k0 + nt * 16) >> (4 * lg);
 #pragma unroll
     for (int jj = 0; jj < EPC; ++jj) {
       const int e = ci * EPC + jj, r = e & 3, nt = (e >> 2) % C::NTK, i = e / (4 * C::NTK), mt = 2 * hf + i;
       const float lv = r == 0 ? l4[i].x : r == 1 ? l4[i].y : r == 2 ? l4[i].z : l4[i].w;
       float x = fmaf(sacc[mt][nt][r], c, lv);
       // (a row of a full block has a finite LSE; a masked pair may have LSE = -inf)
-      if (masked) x = legal32(g, q0 + 4 * lg + mt * 16 + r, k0 + nt * 16) ? x : -INFINITY;
+      if (masked) {
+        const uint32_t m = (uint32_t)((int32_t)(qmask[nt] << (31 - (16 * i + r))) >> 31);
+        x = __uint_as_float((__float_as_uint(x) & m) | (0xff800000u & ~m));
+      }
       const float pv = __builtin_amdgcn_exp2f(x);
       pb[hf][nt][4 * i + r] = (__bf16)pv;
       sb[hf][nt][4 * i + r] = (__bf16)(pv * pacc[mt][nt][r]);

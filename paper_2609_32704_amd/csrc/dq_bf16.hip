@@ -231,19 +231,18 @@ __global__ void __launch_bounds__(256) bwd_dq32(cowa_params p, SchedView sv, con
   const float c = p.softmax_scale * kLog2e;
 
   float pv[16 * NQT];  // exponentials in flight between the two halves of an element step
+  uint32_t lmask[NQT];  // legal keys of the chunk being masked, per query tile
   // element step e of a chunk (query tile e / 16, slot e % 16), first half: P
   auto soft_a = [&](auto ec, auto rpc, bool masked, int key0) __attribute__((always_inline)) {
     constexpr int e = decltype(ec)::value, rp = decltype(rpc)::value;
     constexpr int nq = e / 16, s = e % 16;
     if (masked) {  // key0: this lane's first key of the chunk
+      // the window rule as a bit mask over the lane's keys key0 .. key0 + 31,
+      // once per chunk and query tile (slot s holds key key0 + cs)
       constexpr int cs = 8 * (s >> 2) + (s & 3);
-      const int qq = q_first + nq * 32 + l32;
-      int dq_ = qq + g.off - key0;
-      asm("" : "+v"(dq_));
-      const int dd = dq_ - cs, kk = key0 + cs;
-      const bool ok = (qq < g.n_q) & (kk < g.n_k) & (dd >= 0) &
-                      ((dd < g.w_near) | (kk < g.w_sink) | ((dd >= g.lo) & (dd < g.hi)));
-      sacc[rp][nq][s] += ok ? 0.f : -INFINITY;
+      if constexpr (s == 0) lmask[nq] = legal_keys32(g, q_first + nq * 32 + l32, key0);
+      const uint32_t m = (uint32_t)((int32_t)(lmask[nq] << (31 - cs)) >> 31);
+      sacc[rp][nq][s] = __uint_as_float((__float_as_uint(sacc[rp][nq][s]) & m) | (0xff800000u & ~m));
     }
     pv[e] = __builtin_amdgcn_exp2f(fmaf(sacc[rp][nq][s], c, mlse[nq]));
   };

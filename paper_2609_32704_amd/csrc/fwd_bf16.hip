@@ -264,21 +264,19 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   const bf16x2 ones = {(__bf16)1.f, (__bf16)1.f};
 
   float pv[32];  // exponentials in flight between the two halves of an element step
+  uint32_t lmask[NQT];  // legal keys of the chunk being masked, per query tile
   // element step e of a chunk's softmax (query tile e / 16, slot e % 16), first half
   auto soft_a = [&](auto ec, auto rpc, bool masked, int key0) __attribute__((always_inline)) {
     constexpr int e = decltype(ec)::value, rp = decltype(rpc)::value;
     constexpr int nq = e / 16, s = e % 16;
     if (masked) {  // key0: this lane's first key of the chunk
-      // the window rule with the distance taken once per chunk and query tile
-      // (kept opaque, so the compiler does not precompute a distance per slot)
+      // the window rule as a bit mask over the lane's keys key0 .. key0 + 31,
+      // once per chunk and query tile; slot s holds key key0 + cs, which an
+      // illegal pair turns into -inf (bit select, no compare)
       constexpr int cs = 8 * (s >> 2) + (s & 3);
-      const int qq = q_first + nq * 32 + l32;
-      int dq = qq + g.off - key0;
-      asm("" : "+v"(dq));
-      const int d = dq - cs, kk = key0 + cs;
-      const bool ok = (qq < g.n_q) & (kk < g.n_k) & (d >= 0) &
-                      ((d < g.w_near) | (kk < g.w_sink) | ((d >= g.lo) & (d < g.hi)));
-      sacc[rp][nq][s] += ok ? 0.f : -INFINITY;
+      if constexpr (s == 0) lmask[nq] = legal_keys32(g, q_first + nq * 32 + l32, key0);
+      const uint32_t m = (uint32_t)((int32_t)(lmask[nq] << (31 - cs)) >> 31);
+      sacc[rp][nq][s] = __uint_as_float((__float_as_uint(sacc[rp][nq][s]) & m) | (0xff800000u & ~m));
     }
     pv[e] = __builtin_amdgcn_exp2f(fmaf(sacc[rp][nq][s], c, -mu[nq]));
   };
@@ -324,7 +322,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
       need |= e > kLimit - kHead;
       hot |= e > kHot;
     }
-    if (__ballot(need) == 0) return;
+    if (__builtin_expect(__ballot(need) == 0, 1)) return;  // (rare: keep it a branch)
     constexpr int PS = (NCH - 2) & 1;  // pair buffer of the pending chunk
 #pragma unroll
     for (int nq = 0; nq < NQT; ++nq) {

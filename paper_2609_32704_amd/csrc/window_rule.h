@@ -87,6 +87,39 @@ __host__ __device__ inline bool legal32(const Geo32& g, int32_t q, int32_t k) {
   return (q < g.n_q) & (k < g.n_k) & (d >= 0) & ((d < g.w_near) | (k < g.w_sink) | ((d >= g.lo) & (d < g.hi)));
 }
 
+// Bits a..b (inclusive) of a 32-bit word, for any a, b (none when a > b or the
+// range misses 0..31).
+__host__ __device__ inline uint32_t bit_range32(int32_t a, int32_t b) {
+  const int32_t lo = a < 0 ? 0 : (a > 32 ? 32 : a);
+  const int32_t hi = b < 0 ? 0 : (b > 31 ? 32 : b + 1);
+  const int32_t w = hi - lo;  // (32-bit arithmetic only: few registers)
+  return w <= 0 ? 0u : (w >= 32 ? ~0u : ((1u << (w & 31)) - 1u) << (lo & 31));
+}
+__host__ __device__ inline int32_t imin32(int32_t a, int32_t b) { return a < b ? a : b; }
+__host__ __device__ inline int32_t imax32(int32_t a, int32_t b) { return a > b ? a : b; }
+
+// legal32 over 32 consecutive keys at once: bit j is legal32(g, q, key0 + j).
+// For one query the legal keys are the union of three runs (near, long, sink)
+// cut to d >= 0 and k < n_k; each run becomes a range of bits, so a partial
+// block's element mask costs a few operations per query and chunk instead of
+// the window rule per element.
+__host__ __device__ inline uint32_t legal_keys32(const Geo32& g, int32_t q, int32_t key0) {
+  const int32_t d0 = q + g.off - key0;                // distance of key0
+  const int32_t up = imin32(d0, g.n_k - 1 - key0);    // d >= 0, k < n_k
+  const uint32_t m = bit_range32(d0 - g.w_near + 1, up) | bit_range32(d0 - g.hi + 1, imin32(up, d0 - g.lo)) |
+                     bit_range32(0, imin32(up, g.w_sink - 1 - key0));
+  return q < g.n_q ? m : 0u;  // (a select, not a branch)
+}
+// The same over 32 consecutive queries for one key: bit i is legal32(g, q0 + i, k).
+__host__ __device__ inline uint32_t legal_queries32(const Geo32& g, int32_t q0, int32_t k) {
+  const int32_t e0 = q0 + g.off - k;                  // distance of query q0
+  const int32_t up = g.n_q - 1 - q0;                  // q < n_q
+  const uint32_t m = bit_range32(-e0, imin32(up, g.w_near - 1 - e0)) |
+                     bit_range32(imax32(-e0, g.lo - e0), imin32(up, g.hi - 1 - e0)) |
+                     (k < g.w_sink ? bit_range32(-e0, up) : 0u);
+  return k < g.n_k ? m : 0u;
+}
+
 // Up to three inclusive ranges, merged (overlapping or adjacent ranges join).
 struct Ranges {
   int32_t n;
