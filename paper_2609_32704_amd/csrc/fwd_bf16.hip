@@ -530,7 +530,12 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
       stage(kbase, 0, kbuf_off(0));
       if (NCH == 4) stage(vbase, 0, vbuf_off(0));  // (needed from the block's third chunk)
     }
-    __builtin_amdgcn_s_waitcnt(0);
+    // K of the first block has landed; with 128-key blocks and full waves its V
+    // may still be in flight (the first block's mid-block wait covers it)
+    if constexpr (NCH == 4 && FULL)
+      __builtin_amdgcn_s_waitcnt(vmcnt_only(PPW));
+    else
+      __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (pass == 0 && n_ent > 0) {
       // offsets from the first 32 keys of the row's first block (in processing
