@@ -552,9 +552,10 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
 #pragma unroll
       for (int nq = 0; nq < NQT; ++nq) {
         float cm = -INFINITY;
+        const uint32_t lm = legal_keys32(g, q_first + nq * 32 + l32, kb);
 #pragma unroll
         for (int x = 0; x < 16; ++x) {
-          const bool ok = legal32(g, q_first + nq * 32 + l32, kb + 8 * (x >> 2) + (x & 3));
+          const bool ok = (lm >> (8 * (x >> 2) + (x & 3))) & 1u;
           cm = fmaxf(cm, ok ? sacc[0][nq][x] : -INFINITY);
         }
         cm = fmaxf(cm, __shfl_xor(cm, 32));
