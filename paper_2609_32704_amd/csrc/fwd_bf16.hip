@@ -328,13 +328,18 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
     for (int nq = 0; nq < NQT; ++nq) {
       const float mh = fmaxf(m_hi[nq], __shfl_xor(m_hi[nq], 32)) * c + kHead;
       const bool mv = mh > mu[nq] + kLimit;
-      const float f = mv ? __builtin_amdgcn_exp2f(mu[nq] - mh) : 1.f;
+      // the factor 2^(m_old - m) is applied as its square root twice: a jump of
+      // the maximum by more than 126 within one block would make it underflow,
+      // although the products (the new maximum's own terms among them) are
+      // ordinary numbers; the square root stays normal up to a jump of 252,
+      // beyond which P has overflowed and the row runs again anyway
+      const float f = mv ? __builtin_amdgcn_exp2f(0.5f * (mu[nq] - mh)) : 1.f;
       mu[nq] = mv ? mh : mu[nq];
-      l_run[nq] *= f;
+      l_run[nq] = l_run[nq] * f * f;
 #pragma unroll
       for (int md = 0; md < MD; ++md) {  // one tile at a time, back into its AGPRs
 #pragma unroll
-        for (int x = 0; x < 16; ++x) oacc[md][nq][x] *= f;
+        for (int x = 0; x < 16; ++x) oacc[md][nq][x] = oacc[md][nq][x] * f * f;
         asm volatile("" : "+a"(oacc[md][nq]));
       }
 #pragma unroll
@@ -345,7 +350,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
           // expression itself reads element 0)
           const uint32_t u = pbw[PS][kk][nq][w];
           const bf16x2 pk = __builtin_bit_cast(bf16x2, u);
-          const bf16x2 sc2 = {(__bf16)((float)pk[0] * f), (__bf16)((float)pk[1] * f)};
+          const bf16x2 sc2 = {(__bf16)((float)pk[0] * f * f), (__bf16)((float)pk[1] * f * f)};
           pbw[PS][kk][nq][w] = __builtin_bit_cast(uint32_t, sc2);
         }
     }

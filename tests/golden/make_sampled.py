@@ -21,7 +21,12 @@ Sample (per workload):
   (w_sink <= i_k < N_k - lo_h), and the last key.  Each key row is exact: every
   query that sees it is evaluated over its whole visible set (Alg. 2).
 
-Usage: python tests/golden/make_sampled.py [bf16_t32k_b2] [bf16_t128k]
+A third sample, ``bf16_t128k_wide``, takes the 128K workload with Q scaled
+by 32 (exact in bf16: a power of two), so that the softmax of most rows spans
+far more than the forward's exponent headroom; it stores O and LSE of the same
+kind of query sample (forward only).
+
+Usage: python tests/golden/make_sampled.py [bf16_t32k_b2] [bf16_t128k] [bf16_t128k_wide]
 Writes tests/golden/sampled_<workload>.npz (float32 values, int64 indices).
 """
 
@@ -121,7 +126,31 @@ def make(name):
     log(f"  wrote {out} ({os.path.getsize(out) / 1e6:.1f} MB)")
 
 
+WIDE_SCALE = 32.0  # Q multiplier of the wide-score sample
+
+
+def make_wide(name="bf16_t128k_wide", base="bf16_t128k"):
+    w = inputs.WORKLOADS[base]
+    rng = np.random.default_rng(inputs.key_of("golden", name))
+    blocks, q_rows = sample_query_rows(w, rng)
+    log(f"{name}: {len(blocks)} QO blocks {blocks}, {len(q_rows)} query rows")
+    t0 = time.perf_counter()
+    t = inputs.train_tensors(w, which=("q", "k", "v"))
+    q, k, v = (t[n][1] for n in ("q", "k", "v"))
+    del t
+    q = q * WIDE_SCALE
+    log(f"  inputs: {time.perf_counter() - t0:.1f} s")
+    t0 = time.perf_counter()
+    o, lse = ref.forward_rows(q, k, v, q_rows, w.w_sink, w.w_near, w.scale)
+    log(f"  query rows: {time.perf_counter() - t0:.1f} s")
+    out = os.path.join(HERE, f"sampled_{name}.npz")
+    np.savez(out, workload=np.array(name), base=np.array(base), q_scale=np.array(WIDE_SCALE),
+             q_rows=np.array(q_rows, dtype=np.int64), o=o.astype(np.float32), lse=lse.astype(np.float32),
+             q_blocks=np.array(blocks, dtype=np.int64))
+    log(f"  wrote {out} ({os.path.getsize(out) / 1e6:.1f} MB)")
+
+
 if __name__ == "__main__":
-    names = sys.argv[1:] or ["bf16_t32k_b2", "bf16_t128k"]
+    names = sys.argv[1:] or ["bf16_t32k_b2", "bf16_t128k", "bf16_t128k_wide"]
     for n in names:
-        make(n)
+        make_wide(n) if n == "bf16_t128k_wide" else make(n)

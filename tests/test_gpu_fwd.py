@@ -83,14 +83,16 @@ def test_fwd_deterministic():
 
 
 @pytest.mark.parametrize("lift,lse_min,d,tile", [(4.0, 60.0, 64, 128), (9.0, 130.0, 64, 128), (4.0, 60.0, 64, 64),
-                                                 (9.0, 130.0, 64, 64), (3.0, 60.0, 128, 64), (3.0, 60.0, 128, 128)])
+                                                 (9.0, 130.0, 64, 64), (3.0, 60.0, 128, 64), (3.0, 60.0, 128, 128),
+                                                 (6.5, 90.0, 64, 128), (6.5, 90.0, 64, 64)])
 def test_fwd_wide_score_range(lift, lse_min, d, tile):
     """Keys of the second 128-key block score far above the rest, so rows whose
     first processed block is another one pass the forward's starting exponent
     offset by a wide margin.  lift 4 (about 90 in log2 units): the offset moves
     at the end of that block and O, l and the pending P are rescaled once.
     lift 9 (about 200): P overflows within the block, and the row runs its
-    second pass with the row maximum.  With 64-key blocks the pending P^T at a
+    second pass with the row maximum.  lift 6.5 (about 150): no overflow, but
+    the rescale factor 2^(m_old - m) alone would underflow.  With 64-key blocks the pending P^T at a
     block end is the block's first chunk instead of its third.  The fp64 oracle
     has no offset at all."""
     dev = need_gpu()

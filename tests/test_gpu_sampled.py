@@ -79,3 +79,32 @@ def test_sampled_bf16_t32k_b2():
 
 def test_sampled_bf16_t128k():
     _sampled("bf16_t128k")
+
+
+def test_sampled_bf16_t128k_wide_scores():
+    """The 128K forward with Q scaled by 32 (exact in bf16), against stored
+    oracle O and LSE: most rows' scores climb far past the forward's starting
+    exponent offset, so the offset moves at block ends (and in rare rows the
+    row runs again); the fp64 oracle has no offset."""
+    import paper_2609_32704_amd as cowa
+    dev = need_gpu()
+    g = _golden("bf16_t128k_wide")
+    w = inputs.WORKLOADS[str(g["base"])]
+    scale_q = float(g["q_scale"])
+    log(f"bf16_t128k_wide: generating inputs (Q x {scale_q:g})")
+    t = inputs.train_tensors(w, which=("q", "k", "v"), values=False)
+    q, k, v = (to_dev(t[n][0], dev) for n in ("q", "k", "v"))
+    del t
+    q = (q.float() * scale_q).to(torch.bfloat16)  # exact: a power of two
+    o = torch.full_like(q, float("nan"))
+    lse = torch.full((w.batch, w.h_q, w.n_q), float("nan"), dtype=torch.float32, device=dev)
+    log("bf16_t128k_wide: forward on the device")
+    cowa.fwd(q, k, v, w.w_sink, w.w_near, w.tile, w.tile, w.scale, out=o, lse=lse)
+    torch.cuda.synchronize()
+    assert not torch.isnan(o).any().item() and not torch.isnan(lse).any().item()
+    rows = torch.from_numpy(g["q_rows"]).to(dev)
+    b, h, i = rows[:, 0], rows[:, 1], rows[:, 2]
+    log(f"bf16_t128k_wide: {len(rows)} query rows on {len(g['q_blocks'])} QO blocks x {w.h_q} QO heads")
+    assert float(g["lse"].max()) > 100.0  # the score range of the case (natural log)
+    compare("O", to_host(o[b, h, i]), g["o"])
+    compare("LSE", lse[b, h, i].cpu().numpy().astype(np.float64), g["lse"])
