@@ -465,9 +465,10 @@ def main():
                 workloads[f"tp8_rank{r}"] = dict(
                     time_train(par, q[:, :4], k[:, :1], v[:, :1], do[:, :4], 5),
                     shape=f"131072 tokens, one rank of 8: global KV head {r}, 4 QO heads")
-            # the forward with a wide score range: Q scaled by 40, so that in most rows a later
-            # score exceeds the exponent offset fixed from the row's first 32 keys by more than
-            # 2^64 and the row runs a second pass (the worst case of the fixed-offset softmax)
+            # the forward with a wide score range: Q scaled by 40, so that in most rows later
+            # scores climb far past the row's first 32 keys: the exponent offset moves at block
+            # ends several times per row, and rows whose maximum jumps past the headroom within
+            # one block run a second pass (the worst case of the forward's softmax offset)
             qw = (q.float() * 40.0).to(torch.bfloat16)
             ow = torch.empty_like(qw)
             tw = 0.0
@@ -482,7 +483,8 @@ def main():
                     tw += e[0].elapsed_time(e[1]) / 3
             workloads["fwd_wide_scores"] = {
                 "fwd_ms": tw, "fwd_ms_normal_scores": per["fwd"], "slowdown": tw / per["fwd"],
-                "shape": "the 131072-token forward with Q scaled by 40 (most rows run the second pass)"}
+                "shape": "the 131072-token forward with Q scaled by 40 (the softmax offset moves often; "
+                         "a few rows run the second pass)"}
             del qw, ow
 
     dense = None
