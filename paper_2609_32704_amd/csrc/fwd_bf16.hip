@@ -17,14 +17,17 @@
 //     B-operand layout of P^T for O^T += V^T P^T, so P never leaves registers;
 //     the V^T fragments come from the row-major V_j through the transposing
 //     LDS read (ds_read_b64_tr_b16).
-//   * only blocks flagged partial evaluate the element mask of Eq. fwa_support;
-//   * softmax in base 2 with a per-row fixed exponent offset (see below), the
-//     scale * log2(e) folded into one fused multiply-add per score, and the
-//     row sum l accumulated from the rounded bf16 P that enters O;
+//   * only blocks flagged partial apply the element mask of Eq. fwa_support,
+//     as a 32-bit mask of legal keys per query and chunk;
+//   * softmax in base 2 with a per-row exponent offset that moves only at
+//     block ends and rarely (see below), the scale * log2(e) folded into one
+//     fused multiply-add per score, and the row sum l accumulated from the
+//     rounded bf16 P that enters O;
 //   * the 32-key chunks of a row form a software pipeline: S^T of chunk n and
 //     O^T of chunk n - 2 on the matrix cores while the vector ALUs exponentiate
 //     chunk n - 1.
-// Finally O = O / l and LSE = (m + log2 l) ln 2 (natural log).
+// Finally O = O / l and LSE = (m + log2 l) ln 2 (natural log); O leaves through
+// LDS as whole rows.
 #include "internal.h"
 #include "window_rule.h"
 #include "mfma_tiles.h"
