@@ -22,7 +22,9 @@
 //   * softmax in base 2 with a per-row exponent offset that moves only at
 //     block ends and rarely (see below), the scale * log2(e) folded into one
 //     fused multiply-add per score, and the row sum l accumulated from the
-//     rounded bf16 P that enters O;
+//     rounded bf16 P^T that enters O, on the matrix cores (one 16x16x32
+//     product per 16 keys with a 0/1 selector as A), which keeps the vector
+//     ALUs, the busier unit, for the exponentials;
 //   * the 32-key chunks of a row form a software pipeline: S^T of chunk n and
 //     O^T of chunk n - 2 on the matrix cores while the vector ALUs exponentiate
 //     chunk n - 1.
@@ -260,11 +262,25 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   // set from the row maximum found by the first pass, as it does when m was
   // unset (no legal key among the first 32) but the row has legal keys.
   constexpr float kHead = 64.f, kLimit = 32.f;
-  float m_fix[NQT], m_hi[NQT], l_run[NQT], mu[NQT];  // m_hi: this lane's maximum raw score per column
+  float m_fix[NQT], m_hi[NQT], mu[NQT];  // m_hi: this lane's maximum raw score per column
 #pragma unroll
   for (int nq = 0; nq < NQT; ++nq) m_fix[nq] = -INFINITY;
   const float c = p.softmax_scale * kLog2e;
-  const bf16x2 ones = {(__bf16)1.f, (__bf16)1.f};
+  // Row sums l = sum of the rounded P^T over the keys, per query column, on the
+  // matrix cores: the P^T fragment of a 16-key k-step, read as the B operand of
+  // a 16x16x32 product, holds in lane L column L % 16 of k-group L / 16, which
+  // is query 32 nq + (L % 32) with the keys of half L / 32.  A selector A with
+  // ones where (row < 8) equals (k-group even) adds, into rows 0-7, the two
+  // k-groups of queries 0-15 and, into rows 8-15, those of queries 16-31.  Lane
+  // L then holds the sum of query column lcol in all four slots; the sum of
+  // lane L's own column is in lane lsrc.
+  f32x4 lacc[NQT];
+  const bf16x8 lsel = ((lane & 15) < 8) == (((lane >> 4) & 1) == 0)
+                          ? bf16x8{(__bf16)1.f, (__bf16)1.f, (__bf16)1.f, (__bf16)1.f,
+                                   (__bf16)1.f, (__bf16)1.f, (__bf16)1.f, (__bf16)1.f}
+                          : bf16x8{};
+  const int lcol = (lane & 15) + ((lane & 32) >> 1);
+  const int lsrc = l32 + (l32 & 16);
 
   float pv[32];  // exponentials in flight between the two halves of an element step
   uint32_t lmask[NQT];  // legal keys of the chunk being masked, per query tile
@@ -283,14 +299,13 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
     }
     pv[e] = __builtin_amdgcn_exp2f(fmaf(sacc[rp][nq][s], c, -mu[nq]));
   };
-  // second half (odd e): running maximum, bf16 pair, row sum
+  // second half (odd e): running maximum, bf16 pair
   auto soft_b = [&](auto ec, auto rpc, auto psc) __attribute__((always_inline)) {
     constexpr int e = decltype(ec)::value, rp = decltype(rpc)::value, ps = decltype(psc)::value;
     constexpr int nq = e / 16, s = e % 16;
     if constexpr (s & 1) {
       m_hi[nq] = max3(m_hi[nq], sacc[rp][nq][s - 1], sacc[rp][nq][s]);
       const bf16x2 pk = {(__bf16)pv[e - 1], (__bf16)pv[e]};
-      l_run[nq] = __builtin_amdgcn_fdot2_f32_bf16(pk, ones, l_run[nq], false);  // l from the rounded P
       pbw[ps][s / 8][nq][(s & 7) >> 1] = __builtin_bit_cast(uint32_t, pk);
     }
   };
@@ -338,7 +353,10 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
       // beyond which P has overflowed and the row runs again anyway
       const float f = mv ? __builtin_amdgcn_exp2f(0.5f * (mu[nq] - mh)) : 1.f;
       mu[nq] = mv ? mh : mu[nq];
-      l_run[nq] = l_run[nq] * f * f;
+      {
+        const float fl = __shfl(f, lcol);  // the factor of the column whose sum this lane holds
+        lacc[nq] = lacc[nq] * fl * fl;     // (one factor at a time, as for O below)
+      }
 #pragma unroll
       for (int md = 0; md < MD; ++md) {  // one tile at a time, back into its AGPRs
 #pragma unroll
@@ -444,6 +462,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
         } else if constexpr (!(FIRST && OLD)) {
           constexpr int kk = x / MD, md = x % MD;
           oacc[md][m] = mfma32(a, __builtin_bit_cast(bf16x8, pbw[j & 1][kk][m]), oacc[md][m]);
+          if constexpr (md == 0) lacc[m] = mfma16(lsel, __builtin_bit_cast(bf16x8, pbw[j & 1][kk][m]), lacc[m]);
         }
         // the softmax of the chunk before chunk j (chunk j - 1 of this block,
         // or the last chunk of the previous block), spread over the products
@@ -505,6 +524,10 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
 #pragma unroll
       for (int nq = 0; nq < NQT; ++nq)
         oacc[md][nq] = mfma32(a, __builtin_bit_cast(bf16x8, pbw[jo & 1][kk][nq]), oacc[md][nq]);
+      if constexpr (md == 0)
+#pragma unroll
+        for (int nq = 0; nq < NQT; ++nq)
+          lacc[nq] = mfma16(lsel, __builtin_bit_cast(bf16x8, pbw[jo & 1][kk][nq]), lacc[nq]);
     });
   };
   using TT = std::true_type;
@@ -530,7 +553,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
 #pragma unroll
     for (int nq = 0; nq < NQT; ++nq) {
       m_hi[nq] = -INFINITY;
-      l_run[nq] = 0.f;
+      lacc[nq] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int md = 0; md < MD; ++md) oacc[md][nq] = f32x16{};
     }
@@ -586,7 +609,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
     if (__ballot(hot) != 0) {
 #pragma unroll
       for (int nq = 0; nq < NQT; ++nq) {
-        far |= !__builtin_isfinite(l_run[nq]);
+        far |= !__builtin_isfinite(lacc[nq][0]);
 #pragma unroll
         for (int md = 0; md < MD; ++md) {
 #pragma unroll
@@ -615,7 +638,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   unsigned char* ot = smem + wave * C::NQW * OP;
 #pragma unroll
   for (int nq = 0; nq < NQT; ++nq) {
-    const float lt = l_run[nq] + __shfl_xor(l_run[nq], 32);
+    const float lt = __shfl(lacc[nq][0], lsrc);
     const int qp = q_first + nq * 32 + l32;
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
 #pragma unroll
