@@ -269,18 +269,16 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   // Row sums l = sum of the rounded P^T over the keys, per query column, on the
   // matrix cores: the P^T fragment of a 16-key k-step, read as the B operand of
   // a 16x16x32 product, holds in lane L column L % 16 of k-group L / 16, which
-  // is query 32 nq + (L % 32) with the keys of half L / 32.  A selector A with
-  // ones where (row < 8) equals (k-group even) adds, into rows 0-7, the two
-  // k-groups of queries 0-15 and, into rows 8-15, those of queries 16-31.  Lane
-  // L then holds the sum of query column lcol in all four slots; the sum of
-  // lane L's own column is in lane lsrc.
+  // is query 32 nq + (L % 32) with the keys of half L / 32 (k-groups 0 and 2:
+  // queries 0-15, 1 and 3: queries 16-31).  The selector A has ones where
+  // (row & 4) == 0 equals (k-group even), so rows 0-3 and 8-11 sum queries 0-15
+  // and rows 4-7 and 12-15 queries 16-31; the result rows 4 (L / 16) .. + 3 of
+  // lane L then all hold the sum of lane L's own query column L % 32.
   f32x4 lacc[NQT];
-  const bf16x8 lsel = ((lane & 15) < 8) == (((lane >> 4) & 1) == 0)
+  const bf16x8 lsel = ((lane & 4) == 0) == (((lane >> 4) & 1) == 0)
                           ? bf16x8{(__bf16)1.f, (__bf16)1.f, (__bf16)1.f, (__bf16)1.f,
                                    (__bf16)1.f, (__bf16)1.f, (__bf16)1.f, (__bf16)1.f}
                           : bf16x8{};
-  const int lcol = (lane & 15) + ((lane & 32) >> 1);
-  const int lsrc = l32 + (l32 & 16);
 
   float pv[32];  // exponentials in flight between the two halves of an element step
   uint32_t lmask[NQT];  // legal keys of the chunk being masked, per query tile
@@ -353,10 +351,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
       // beyond which P has overflowed and the row runs again anyway
       const float f = mv ? __builtin_amdgcn_exp2f(0.5f * (mu[nq] - mh)) : 1.f;
       mu[nq] = mv ? mh : mu[nq];
-      {
-        const float fl = __shfl(f, lcol);  // the factor of the column whose sum this lane holds
-        lacc[nq] = lacc[nq] * fl * fl;     // (one factor at a time, as for O below)
-      }
+      lacc[nq] = lacc[nq] * f * f;
 #pragma unroll
       for (int md = 0; md < MD; ++md) {  // one tile at a time, back into its AGPRs
 #pragma unroll
@@ -638,7 +633,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   unsigned char* ot = smem + wave * C::NQW * OP;
 #pragma unroll
   for (int nq = 0; nq < NQT; ++nq) {
-    const float lt = __shfl(lacc[nq][0], lsrc);
+    const float lt = lacc[nq][0];
     const int qp = q_first + nq * 32 + l32;
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
 #pragma unroll
