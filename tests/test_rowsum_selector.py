@@ -14,8 +14,8 @@ of P over the sixteen keys for lane L's own query column L % 32.
 
 The operand layouts are the ones the kernels are built on (the dK/dV pass
 uses the same 16x16x32 layout, the forward and the dQ pass the 32x32x16 one);
-the GPU parity tests check the kernel itself.  A selector that is off by one k-group or row block, or
-that mixes the two 16-column halves, fails here."""
+the GPU parity tests check the kernel itself.  A selector that is off by one
+k-group or row block, or that mixes the two 16-column halves, fails here."""
 
 import numpy as np
 
