@@ -106,7 +106,7 @@ struct FwdCfg {
 
 // FULL: launched with NWF waves (the fast copy path; a compile-time choice
 // keeps the block step free of branches)
-template <int D, int BQ, int BK, bool FULL>
+template <int D, int BQ, int BK, bool FULL, bool TRACK>
 __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView sv, int hpw,
                                                        const __bf16* __restrict__ q, const __bf16* __restrict__ k,
                                                        const __bf16* __restrict__ v, __bf16* __restrict__ o,
@@ -141,6 +141,19 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   // Q^T fragments (B operands): query column 32 nq + l32, d = 16 ks + 8 hh + 0..7;
   // loaded first, so that their latency overlaps that of the entry lists
   const int64_t row_base = sc.q0 + (int64_t)hq * sc.qh;
+  if constexpr (TRACK) {
+    // only the workgroups with a row that the untracked launch left to this
+    // one (LSE = NaN) run; the rest end here, uniformly
+    int* flag = reinterpret_cast<int*>(smem + C::MAIN_BYTES + 4 * sv.max_kt);
+    if (tid == 0) *flag = 0;
+    __syncthreads();
+    const int qr = q_first + lane;
+    if (__ballot(qr < n_q && __builtin_isnan(lse[row_base + qr])) != 0 && lane == 0) *flag = 1;
+    __syncthreads();
+    const bool mine = *flag != 0;
+    __syncthreads();
+    if (!mine) return;
+  }
   bf16x8 qf[NQT][KS];
 #pragma unroll
   for (int nq = 0; nq < NQT; ++nq) {
@@ -153,6 +166,15 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
       qf[nq][ks] = ok ? val : bf16x8{};
     }
   }
+  // Move the Q^T fragments into AGPRs here, long before the first product: the
+  // assembly products read them from AGPRs, and the compiler could otherwise
+  // copy them there just before that read, without the wait states a product
+  // needs after a vector write of its operands.  (These statements emit
+  // nothing themselves.)
+#pragma unroll
+  for (int nq = 0; nq < NQT; ++nq)
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) asm volatile("" : "+a"(qf[nq][ks]));
   // zero the K/V buffers once when the last KV block is partial: key rows past
   // the end of the sequence are not copied and must hold finite values
   if (n_k % BK != 0)
@@ -297,12 +319,12 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
     }
     pv[e] = __builtin_amdgcn_exp2f(fmaf(sacc[rp][nq][s], c, -mu[nq]));
   };
-  // second half (odd e): running maximum, bf16 pair
+  // second half (odd e): running maximum (TRACK only), bf16 pair
   auto soft_b = [&](auto ec, auto rpc, auto psc) __attribute__((always_inline)) {
     constexpr int e = decltype(ec)::value, rp = decltype(rpc)::value, ps = decltype(psc)::value;
     constexpr int nq = e / 16, s = e % 16;
     if constexpr (s & 1) {
-      m_hi[nq] = max3(m_hi[nq], sacc[rp][nq][s - 1], sacc[rp][nq][s]);
+      if constexpr (TRACK) m_hi[nq] = max3(m_hi[nq], sacc[rp][nq][s - 1], sacc[rp][nq][s]);
       const bf16x2 pk = {(__bf16)pv[e - 1], (__bf16)pv[e]};
       pbw[ps][s / 8][nq][(s & 7) >> 1] = __builtin_bit_cast(uint32_t, pk);
     }
@@ -364,6 +386,52 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
         for (int w = 0; w < 4; ++w) {
           // (a vector element is copied out first: bit-casting the element
           // expression itself reads element 0)
+          const uint32_t u = pbw[PS][kk][nq][w];
+          const bf16x2 pk = __builtin_bit_cast(bf16x2, u);
+          const bf16x2 sc2 = {(__bf16)((float)pk[0] * f * f), (__bf16)((float)pk[1] * f * f)};
+          pbw[PS][kk][nq][w] = __builtin_bit_cast(uint32_t, sc2);
+        }
+    }
+  };
+
+  // The same move without a tracked maximum (TRACK false): the row sum l of a
+  // column bounds each of its P from above, so when it passes 2^(kLimit -
+  // kHead) at a block end (never before some score has passed the first keys'
+  // maximum by 15 or more: at most 2^31 keys of at most 2^-kHead each) the
+  // offset moves by log2 l + kHead, which leaves every P so far at most
+  // 2^-kHead (l itself becomes 2^-kHead) and overshoots the move the maximum
+  // would give by at most log2 of the row length.  Both lanes of a column hold
+  // the same sum, so they move alike.  The sum lags by the chunks not yet in
+  // it (the pending P^T and the last chunk); a P that overflows in the
+  // meantime makes l infinite, and the row is left to the tracked launch.
+  auto rebase_sum = [&]() __attribute__((always_inline)) {
+    bool need = false;
+#pragma unroll
+    for (int nq = 0; nq < NQT; ++nq) {
+      const float l = lacc[nq][0];
+      need |= l > 0x1p-32f;
+      hot |= !(l <= 0x1p64f);
+    }
+    if (__builtin_expect(__ballot(need) == 0, 1)) return;  // (rare: keep it a branch)
+    constexpr int PS = (NCH - 2) & 1;  // pair buffer of the pending chunk
+#pragma unroll
+    for (int nq = 0; nq < NQT; ++nq) {
+      const float l = lacc[nq][0];
+      const bool mv = l > 0x1p-32f && l <= 0x1p64f;  // (an overflowed sum: the row goes to the tracked launch)
+      const float dm = mv ? __log2f(l) + kHead : 0.f;
+      const float f = mv ? __builtin_amdgcn_exp2f(-0.5f * dm) : 1.f;  // applied twice, as above
+      mu[nq] += dm;
+      lacc[nq] = lacc[nq] * f * f;
+#pragma unroll
+      for (int md = 0; md < MD; ++md) {
+#pragma unroll
+        for (int x = 0; x < 16; ++x) oacc[md][nq][x] = oacc[md][nq][x] * f * f;
+        asm volatile("" : "+a"(oacc[md][nq]));
+      }
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
           const uint32_t u = pbw[PS][kk][nq][w];
           const bf16x2 pk = __builtin_bit_cast(bf16x2, u);
           const bf16x2 sc2 = {(__bf16)((float)pk[0] * f * f), (__bf16)((float)pk[1] * f * f)};
@@ -484,7 +552,10 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
     // anything reads them
     mfma_settle(sacc[1]);
     __builtin_amdgcn_sched_barrier(0);
-    rebase();
+    if constexpr (TRACK)
+      rebase();
+    else
+      rebase_sum();
     // register placement: O^T accumulators and Q^T fragments in AGPRs (read
     // directly by the matrix cores), S^T and P^T in VGPRs; these emit nothing
 #pragma unroll
@@ -544,7 +615,11 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
   };
 
   int* vote = reinterpret_cast<int*>(smem + C::MAIN_BYTES + 4 * cap);
-  for (int pass = 0; pass < 2; ++pass) {
+  // TRACK false: one pass without a tracked maximum (its offset moves on the
+  // row sums); rows it cannot finish get LSE = NaN and are run again by the
+  // TRACK launch, with up to two passes as described above
+  bool flagged = false;
+  for (int pass = 0; pass < (TRACK ? 2 : 1); ++pass) {
 #pragma unroll
     for (int nq = 0; nq < NQT; ++nq) {
       m_hi[nq] = -INFINITY;
@@ -591,15 +666,27 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
 #pragma unroll
     for (int nq = 0; nq < NQT; ++nq) mu[nq] = m_fix[nq] == -INFINITY ? 0.f : m_fix[nq] + kHead;
     sweep();
-    // was a column's offset unset although it met legal keys later, or did P,
-    // l or O overflow (possible only after a P above 2^kHot)?
     bool far = false;
+    if constexpr (TRACK) {
+      // was a column's offset unset although it met legal keys later, or did
+      // P, l or O overflow (possible only after a P above 2^kHot)?
 #pragma unroll
-    for (int nq = 0; nq < NQT; ++nq) {
-      hot |= m_hi[nq] * c - mu[nq] > kHot;  // (the last chunk came after the last block end)
-      const float mh = fmaxf(m_hi[nq], __shfl_xor(m_hi[nq], 32)) * c;  // the column maximum, exponent units
-      far |= mh != -INFINITY && m_fix[nq] == -INFINITY;
-      m_fix[nq] = mh;  // the offset of a second pass: then P <= 2^-kHead everywhere
+      for (int nq = 0; nq < NQT; ++nq) {
+        hot |= m_hi[nq] * c - mu[nq] > kHot;  // (the last chunk came after the last block end)
+        const float mh = fmaxf(m_hi[nq], __shfl_xor(m_hi[nq], 32)) * c;  // the column maximum, exponent units
+        far |= mh != -INFINITY && m_fix[nq] == -INFINITY;
+        m_fix[nq] = mh;  // the offset of a second pass: then P <= 2^-kHead everywhere
+      }
+    } else {
+      // a column without an offset at the start (m = 0) keeps its sum only if
+      // that sum is comfortably normal (otherwise it met no legal key, or its
+      // P underflowed); an overflow shows in the sum
+#pragma unroll
+      for (int nq = 0; nq < NQT; ++nq) {
+        const float l = lacc[nq][0];
+        hot |= !(l <= 0x1p64f);
+        far |= m_fix[nq] == -INFINITY && q_first + nq * 32 + l32 < n_q && !(l >= 0x1p-60f);
+      }
     }
     if (__ballot(hot) != 0) {
 #pragma unroll
@@ -621,6 +708,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
     __syncthreads();
     const bool again = *vote != 0;
     __syncthreads();
+    if (!TRACK) flagged = again;
     if (!again) break;
   }
 
@@ -645,7 +733,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
         for (int rr = 0; rr < 4; ++rr) ov[rr] = (__bf16)(oacc[md][nq][4 * j4 + rr] * inv);
         *reinterpret_cast<bf16x4*>(ot + (nq * 32 + l32) * OP + (md * 32 + 8 * j4 + 4 * hh) * 2) = ov;
       }
-    if (hh == 0 && qp < n_q) lse[row_base + qp] = lt > 0.f ? (mu[nq] + __log2f(lt)) * kLn2 : -INFINITY;
+    if (hh == 0 && qp < n_q) lse[row_base + qp] = flagged ? __builtin_nanf("") : lt > 0.f ? (mu[nq] + __log2f(lt)) * kLn2 : -INFINITY;
   }
   constexpr int CPR = D / 8;  // 16-byte chunks per row
 #pragma unroll
@@ -661,13 +749,18 @@ template <int D, int BQ, int BK, bool FULL>
 hipError_t launch_waves(const cowa_params& p, const SchedView& sv, int hpw, int n_hgroups, int waves, const void* q,
                         const void* k, const void* v, void* o, float* lse, hipStream_t stream) {
   using C = FwdCfg<D, BQ, BK>;
-  auto kern = fwd_bf16_kernel<D, BQ, BK, FULL>;
-  {
-    const hipError_t err = allow_lds(reinterpret_cast<const void*>(kern), C::LDS_MAX);
+  // the untracked launch, then the tracked one for the rows it flagged
+  auto kern0 = fwd_bf16_kernel<D, BQ, BK, FULL, false>;
+  auto kern1 = fwd_bf16_kernel<D, BQ, BK, FULL, true>;
+  for (const void* kp : {reinterpret_cast<const void*>(kern0), reinterpret_cast<const void*>(kern1)}) {
+    const hipError_t err = allow_lds(kp, C::LDS_MAX);
     if (err != hipSuccess) return err;
   }
   const unsigned blocks = (unsigned)sv.n_qt * n_hgroups * (sv.ragged ? 1 : p.batch);
-  hipLaunchKernelGGL(kern, dim3(blocks), dim3(64 * waves), C::lds_bytes(sv.max_kt), stream, p, sv, hpw,
+  hipLaunchKernelGGL(kern0, dim3(blocks), dim3(64 * waves), C::lds_bytes(sv.max_kt), stream, p, sv, hpw,
+                     static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), static_cast<const __bf16*>(v),
+                     static_cast<__bf16*>(o), lse);
+  hipLaunchKernelGGL(kern1, dim3(blocks), dim3(64 * waves), C::lds_bytes(sv.max_kt), stream, p, sv, hpw,
                      static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), static_cast<const __bf16*>(v),
                      static_cast<__bf16*>(o), lse);
   return hipGetLastError();
