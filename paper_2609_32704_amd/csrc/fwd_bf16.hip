@@ -417,7 +417,7 @@ __global__ void __launch_bounds__(256) fwd_bf16_kernel(cowa_params p, SchedView 
 #pragma unroll
     for (int nq = 0; nq < NQT; ++nq) {
       const float l = lacc[nq][0];
-      const bool mv = l > 0x1p-32f && l <= 0x1p64f;  // (an overflowed sum: the row goes to the tracked launch)
+      const bool mv = l > 0x1p-32f && l < INFINITY;  // (an overflowed sum: the row goes to the tracked launch)
       const float dm = mv ? __log2f(l) + kHead : 0.f;
       const float f = mv ? __builtin_amdgcn_exp2f(-0.5f * dm) : 1.f;  // applied twice, as above
       mu[nq] += dm;
