@@ -30,6 +30,12 @@
 //     chunk n - 1.
 // Finally O = O / l and LSE = (m + log2 l) ln 2 (natural log); O leaves through
 // LDS as whole rows.
+//
+// Two launches per call (TRACK false, then true).  The first tracks no running
+// maximum: its offset moves on the row sums, and rows it cannot finish (an
+// overflow, or a column without a starting offset whose sum stays tiny) leave
+// LSE = NaN.  The second runs the tracked algorithm described below, but only
+// in workgroups holding such a row; the others end at once.
 #include "internal.h"
 #include "window_rule.h"
 #include "mfma_tiles.h"
